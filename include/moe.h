@@ -1,0 +1,195 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) MoE-layer forward library (libmoe_mi355x.so).
+ *
+ * The library computes the forward pass of one Mixture-of-Experts layer on one
+ * expert-parallel rank's share of the work: router logits, top-k gating, the
+ * per-expert histogram and prefix scan of local (token, expert) pairs, the
+ * permutation of token rows into expert-contiguous order, the grouped SwiGLU
+ * expert MLP (plus an optional shared expert) and the gate-weighted combine.
+ * These are the steps a generated MoE expert kernel performs in the paper's
+ * kernel-generation design (Section 3.1, kernel sub-plan: permute before the
+ * grouped GEMM, weighted combine after it; Section 4, kernel generation: the
+ * monotone [E+1] row-offset array; Section 4, engine registration: the forward
+ * composes the expert MLP's two GEMMs).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers.  Every tensor argument is a DEVICE pointer owned by the caller.
+ *    bf16 tensors are row-major, contiguous, 16-byte aligned; int32 / float
+ *    arrays are contiguous and 4-byte aligned.  The library allocates no device
+ *    memory on any call path; scratch space comes from the caller's workspace,
+ *    whose size moe_workspace_size() returns.
+ *  - Streams.  `stream` is a hipStream_t passed as an opaque pointer (NULL = the
+ *    legacy default stream).  Each call validates its arguments on the host; on
+ *    success it enqueues its kernels on `stream` and returns without waiting.
+ *    No call synchronises the device or reads device memory on the host: the
+ *    number of local rows stays on the device.
+ *  - Errors.  Calls return a moe_status_t.  On any status other than MOE_OK
+ *    nothing was enqueued (except MOE_ERR_HIP, which reports a failed launch),
+ *    and moe_last_error() returns a thread-local message naming the offending
+ *    argument and its value.  There is no silent fallback: an unsupported shape
+ *    is an error, never a slower path.
+ *  - Limits.  d, F and F_shared are multiples of 8 (16-byte rows of bf16);
+ *    1 <= E <= 1024; 1 <= top_k <= min(E, 16); T * top_k < 2^31; E_local <= 1024.
+ *    T == 0 is a valid no-op.  Results for inputs holding Inf or NaN are
+ *    unspecified.
+ *  - Determinism.  Every output is bit-identical from run to run (no floating-
+ *    point atomics anywhere).
+ *
+ * Layouts
+ * -------
+ *    x          [T, d]             bf16  token rows
+ *    w_router   [E, d]             bf16  router weight, logits = x . w_router^T
+ *    bias       [E]                f32   optional softmax-mode router bias (NULL = 0)
+ *    topk_idx   [T, top_k]         i32   chosen GLOBAL expert ids, slot order = key descending
+ *    topk_w     [T, top_k]         f32   gate of each slot
+ *    counts     [E_local]          i32   local slots per local expert
+ *    offsets    [E_local + 1]      i32   exclusive scan of counts (offsets[0] = 0)
+ *    row_token  [cap]              i32   token of each expert-contiguous row (rows >= offsets[E_local] untouched)
+ *    slot_row   [T, top_k]         i32   row of each slot, -1 when the expert is not local
+ *    x_perm     [cap, d]           bf16  x_perm[r] = x[row_token[r]]
+ *    w13        [E_local, 2F, d]   bf16  per local expert: rows [0,F) = W1 (gate), rows [F,2F) = W3 (up)
+ *    w2         [E_local, d, F]    bf16  per local expert down projection
+ *    y_perm     [cap, d]           bf16  expert MLP output of each row
+ *    ws13/ws2   [2F_s, d] / [d, F_s]     shared expert (same packing), applied to every token with weight 1
+ *    out        [T, d]             bf16
+ *  with cap = T * min(top_k, E_local), the most local rows a batch can produce.
+ */
+#ifndef MOE_MI355X_H
+#define MOE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+
+typedef enum moe_status {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = 1,  /* null / misaligned pointer, inconsistent shape field      */
+  MOE_ERR_UNSUPPORTED = 2,  /* a valid request outside the kernels' stated limits        */
+  MOE_ERR_WORKSPACE = 3,    /* ws_bytes smaller than moe_workspace_size() or ws == NULL  */
+  MOE_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed                */
+} moe_status_t;
+
+typedef enum moe_gate {
+  MOE_GATE_SOFTMAX = 0,     /* key = logit + bias; gate = softmax over the chosen keys (renormalize=1)
+                               or over all experts (renormalize=0); times routed_scale   */
+  MOE_GATE_SIGMOID = 1      /* key = sigmoid(logit); gate = key / sum of chosen keys (renormalize=1)
+                               or key (renormalize=0); times routed_scale; no bias        */
+} moe_gate_t;
+
+/* Which call a workspace is sized for (moe_workspace_size). */
+typedef enum moe_ws_kind {
+  MOE_WS_ROUTE = 0,
+  MOE_WS_PERMUTE = 1,
+  MOE_WS_FFN = 2,
+  MOE_WS_LAYER = 3
+} moe_ws_kind_t;
+
+/* Named regions inside a MOE_WS_LAYER workspace (moe_workspace_offset). */
+typedef enum moe_ws_region {
+  MOE_REGION_TOPK_IDX = 0,   /* i32 [T, top_k]   */
+  MOE_REGION_TOPK_W = 1,     /* f32 [T, top_k]   */
+  MOE_REGION_COUNTS = 2,     /* i32 [E_local]    */
+  MOE_REGION_OFFSETS = 3,    /* i32 [E_local+1]  */
+  MOE_REGION_ROW_TOKEN = 4,  /* i32 [cap]        */
+  MOE_REGION_SLOT_ROW = 5,   /* i32 [T, top_k]   */
+  MOE_REGION_X_PERM = 6,     /* bf16 [cap, d]    */
+  MOE_REGION_Y_PERM = 7,     /* bf16 [cap, d]    */
+  MOE_REGION_SHARED_Y = 8,   /* bf16 [T, d] (only when F_shared > 0) */
+  MOE_REGION_COUNT_ = 9
+} moe_ws_region_t;
+
+/* Shape and gating of one MoE layer on one expert-parallel rank (passed by pointer).
+ * The rank holds experts [e_begin, e_begin + E_local) of the E routed experts; a slot
+ * routed elsewhere is dropped from this rank's compute.  With n_group > 1 the E
+ * experts form n_group contiguous groups, a group scores the sum of its two largest
+ * keys, and only experts of the topk_group best groups are eligible.  Top-k ties go
+ * to the lower expert (group) index. */
+typedef struct moe_shape {
+  int64_t T;            /* tokens                                       */
+  int32_t d;            /* hidden size                                  */
+  int32_t E;            /* routed experts of the whole layer            */
+  int32_t top_k;        /* experts per token                            */
+  int32_t e_begin;      /* first local expert                           */
+  int32_t E_local;      /* local experts                                */
+  int32_t F;            /* routed expert FFN width                      */
+  int32_t F_shared;     /* shared expert FFN width, 0 = none            */
+  int32_t gate;         /* moe_gate_t                                   */
+  int32_t n_group;      /* expert groups, 1 = no group limit            */
+  int32_t topk_group;   /* groups kept per token when n_group > 1       */
+  int32_t renormalize;  /* 0 or 1                                       */
+  float routed_scale;   /* multiplies every routed gate                 */
+} moe_shape_t;
+
+/* Library ABI version (MOE_ABI_VERSION of the build). */
+int moe_abi_version(void);
+
+/* Static description of a status code. */
+const char* moe_status_string(int status);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* moe_last_error(void);
+
+/* Bytes of caller workspace the call `kind` needs for `shape` (0 for an invalid shape;
+ * moe_last_error() then says why).  Always a multiple of 256. */
+size_t moe_workspace_size(const moe_shape_t* shape, int kind);
+
+/* Byte offset of a named region inside a MOE_WS_LAYER workspace, so a caller can read
+ * the routing, permutation and intermediate rows of the last moe_layer_forward on that
+ * workspace.  Returns (size_t)-1 for an invalid shape or region. */
+size_t moe_workspace_offset(const moe_shape_t* shape, int region);
+
+/* Router logits, gating and top-k (steps 1-5 of the layer).
+ * Writes topk_idx and topk_w; when keys_out [T, E] f32 is not NULL it also receives
+ * the float32 key every decision was taken on (softmax: logit + bias; sigmoid: the
+ * sigmoid score), so a checker can replay the decision in the same precision.
+ * Logits accumulate bf16 products in float32.  ws: MOE_WS_ROUTE bytes. */
+int moe_route(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+              int32_t* topk_idx, float* topk_w, float* keys_out,
+              void* ws, size_t ws_bytes, void* stream);
+
+/* Histogram, prefix scan and permutation (steps 6-8).
+ * From topk_idx, keeps the slots whose expert lies in [e_begin, e_begin + E_local),
+ * writes counts and the monotone offsets (expert e owns rows [offsets[e], offsets[e+1])),
+ * orders the rows of one expert by ascending token (a stable counting sort), writes
+ * row_token and slot_row, and gathers x_perm[r] = x[row_token[r]] (bit-exact copy).
+ * ws: MOE_WS_PERMUTE bytes. */
+int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x,
+                int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* slot_row,
+                void* x_perm, void* ws, size_t ws_bytes, void* stream);
+
+/* Grouped SwiGLU expert MLP (step 9): for every local expert e and every row r in
+ * [offsets[e], offsets[e+1]):  y_perm[r] = W2_e (silu(W1_e x_perm[r]) * (W3_e x_perm[r])).
+ * The activation is rounded to bf16 before the second GEMM; accumulation is float32.
+ * `offsets` is a device array of E_local + 1 entries (e.g. from moe_permute) and must
+ * satisfy 0 = offsets[0] <= ... <= offsets[E_local] <= cap.  The shared expert is this
+ * call with E_local = 1, F = F_shared and offsets = {0, T} over x.
+ * ws: MOE_WS_FFN bytes. */
+int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets,
+                    const void* w13, const void* w2, void* y_perm,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* Gate-weighted combine (steps 10-11):
+ *   out[t] = bf16( sum over slots j with slot_row[t,j] >= 0 of topk_w[t,j] * y_perm[slot_row[t,j]]
+ *                  + shared_y[t] )
+ * accumulated in float32 in slot order, the shared row (NULL = none) added last, one
+ * round-to-nearest-even to bf16.  A token with no local slot gets shared_y[t] (or 0). */
+int moe_combine(const moe_shape_t* shape, const void* y_perm, const int32_t* slot_row,
+                const float* topk_w, const void* shared_y, void* out, void* stream);
+
+/* The whole layer: route -> permute -> grouped_ffn (+ shared expert) -> combine.
+ * ws13 / ws2 are required when F_shared > 0 and ignored otherwise.
+ * ws: MOE_WS_LAYER bytes; its named regions hold the intermediates afterwards. */
+int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                      const void* w13, const void* w2, const void* ws13, const void* ws2,
+                      void* out, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_MI355X_H */

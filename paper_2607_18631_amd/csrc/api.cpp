@@ -1,0 +1,404 @@
+// C ABI of the MoE-layer forward: argument validation, workspace layout, kernel dispatch.
+// Every entry point validates on the host before touching the GPU, so an invalid call
+// returns its status without any HIP call; a valid call only enqueues work on `stream`.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/moe.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int ok() {
+  g_err.clear();
+  return MOE_OK;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int64_t capacity(const moe_shape_t* s) {
+  return s->T * (int64_t)(s->top_k < s->E_local ? s->top_k : s->E_local);
+}
+
+int check_shape(const moe_shape_t* s) {
+  if (!s) return fail(MOE_ERR_INVALID_ARG, "shape is NULL");
+  if (s->T < 0) return fail(MOE_ERR_INVALID_ARG, "T (%lld) < 0", (long long)s->T);
+  if (s->d <= 0) return fail(MOE_ERR_INVALID_ARG, "d (%d) <= 0", s->d);
+  if (s->d % 8) return fail(MOE_ERR_UNSUPPORTED, "d (%d) %% 8 != 0 (rows must be 16-byte bf16 vectors)", s->d);
+  if (s->E < 1 || s->E > 1024) return fail(MOE_ERR_UNSUPPORTED, "E (%d) outside [1, 1024]", s->E);
+  if (s->top_k < 1 || s->top_k > 16 || s->top_k > s->E)
+    return fail(MOE_ERR_UNSUPPORTED, "top_k (%d) outside [1, min(E=%d, 16)]", s->top_k, s->E);
+  if (s->T * (int64_t)s->top_k >= (int64_t(1) << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "T * top_k (%lld) >= 2^31", (long long)(s->T * s->top_k));
+  if (s->e_begin < 0 || s->E_local < 1 || (int64_t)s->e_begin + s->E_local > s->E)
+    return fail(MOE_ERR_INVALID_ARG, "local slice [e_begin=%d, e_begin+E_local=%d) not inside [0, E=%d)",
+                s->e_begin, s->e_begin + s->E_local, s->E);
+  if (s->F <= 0) return fail(MOE_ERR_INVALID_ARG, "F (%d) <= 0", s->F);
+  if (s->F % 8) return fail(MOE_ERR_UNSUPPORTED, "F (%d) %% 8 != 0", s->F);
+  if (s->F_shared < 0) return fail(MOE_ERR_INVALID_ARG, "F_shared (%d) < 0", s->F_shared);
+  if (s->F_shared % 8) return fail(MOE_ERR_UNSUPPORTED, "F_shared (%d) %% 8 != 0", s->F_shared);
+  if (s->gate != MOE_GATE_SOFTMAX && s->gate != MOE_GATE_SIGMOID)
+    return fail(MOE_ERR_UNSUPPORTED, "gate (%d) is neither MOE_GATE_SOFTMAX nor MOE_GATE_SIGMOID", s->gate);
+  if (s->n_group < 1) return fail(MOE_ERR_INVALID_ARG, "n_group (%d) < 1", s->n_group);
+  if (s->E % s->n_group) return fail(MOE_ERR_INVALID_ARG, "E (%d) %% n_group (%d) != 0", s->E, s->n_group);
+  if (s->n_group > 1) {
+    if (s->n_group > 64) return fail(MOE_ERR_UNSUPPORTED, "n_group (%d) > 64", s->n_group);
+    if (s->E / s->n_group < 2)
+      return fail(MOE_ERR_INVALID_ARG, "group size E/n_group (%d) < 2: a group scores its two largest keys",
+                  s->E / s->n_group);
+    if (s->topk_group < 1 || s->topk_group > s->n_group)
+      return fail(MOE_ERR_INVALID_ARG, "topk_group (%d) outside [1, n_group=%d]", s->topk_group, s->n_group);
+    if ((int64_t)s->topk_group * (s->E / s->n_group) < s->top_k)
+      return fail(MOE_ERR_INVALID_ARG, "topk_group * group size (%d) < top_k (%d)",
+                  s->topk_group * (s->E / s->n_group), s->top_k);
+  }
+  if (s->renormalize != 0 && s->renormalize != 1)
+    return fail(MOE_ERR_INVALID_ARG, "renormalize (%d) is not 0 or 1", s->renormalize);
+  if (!std::isfinite(s->routed_scale)) return fail(MOE_ERR_INVALID_ARG, "routed_scale is not finite");
+  return MOE_OK;
+}
+
+int check_ptr(const void* p, size_t align, const char* name) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(p) % align)
+    return fail(MOE_ERR_INVALID_ARG, "%s (%p) is not %zu-byte aligned", name, p, align);
+  return MOE_OK;
+}
+
+#define CHECK(expr)          \
+  do {                       \
+    int _st = (expr);        \
+    if (_st != MOE_OK) return _st; \
+  } while (0)
+
+// ---- workspace layouts ----
+size_t ws_route(const moe_shape_t* s) { return align_up((size_t)s->T * s->E * sizeof(float)); }
+size_t ws_permute(const moe_shape_t* s) {
+  return 2 * align_up((size_t)moe::permute_blocks(s->T) * s->E_local * sizeof(int32_t));
+}
+size_t ws_ffn(const moe_shape_t* s) { return align_up((size_t)capacity(s) * s->F * sizeof(uint16_t)); }
+
+struct LayerLayout {
+  size_t region[MOE_REGION_COUNT_];
+  size_t logits, perm_ws, act, act_s, total;
+};
+
+LayerLayout layer_layout(const moe_shape_t* s) {
+  LayerLayout L{};
+  const size_t T = (size_t)s->T, k = (size_t)s->top_k, cap = (size_t)capacity(s), d = (size_t)s->d;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  L.region[MOE_REGION_TOPK_IDX] = take(T * k * 4);
+  L.region[MOE_REGION_TOPK_W] = take(T * k * 4);
+  L.region[MOE_REGION_COUNTS] = take((size_t)s->E_local * 4);
+  L.region[MOE_REGION_OFFSETS] = take(((size_t)s->E_local + 1) * 4);
+  L.region[MOE_REGION_ROW_TOKEN] = take(cap * 4);
+  L.region[MOE_REGION_SLOT_ROW] = take(T * k * 4);
+  L.region[MOE_REGION_X_PERM] = take(cap * d * 2);
+  L.region[MOE_REGION_Y_PERM] = take(cap * d * 2);
+  L.region[MOE_REGION_SHARED_Y] = take(s->F_shared > 0 ? T * d * 2 : 0);
+  L.logits = take(ws_route(s));
+  L.perm_ws = take(ws_permute(s));
+  L.act = take(ws_ffn(s));
+  L.act_s = take(s->F_shared > 0 ? T * (size_t)s->F_shared * 2 : 0);
+  L.total = off;
+  return L;
+}
+
+size_t ws_need(const moe_shape_t* s, int kind) {
+  switch (kind) {
+    case MOE_WS_ROUTE: return ws_route(s);
+    case MOE_WS_PERMUTE: return ws_permute(s);
+    case MOE_WS_FFN: return ws_ffn(s);
+    case MOE_WS_LAYER: return layer_layout(s).total;
+    default: return 0;
+  }
+}
+
+int check_ws(const moe_shape_t* s, int kind, const void* ws, size_t ws_bytes) {
+  const size_t need = ws_need(s, kind);
+  if (need == 0) return MOE_OK;
+  if (!ws) return fail(MOE_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign)
+    return fail(MOE_ERR_INVALID_ARG, "workspace (%p) is not %zu-byte aligned", ws, kAlign);
+  if (ws_bytes < need) return fail(MOE_ERR_WORKSPACE, "ws_bytes (%zu) < required (%zu)", ws_bytes, need);
+  return MOE_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MOE_OK;
+  return fail(MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+template <class T>
+inline T* at(void* base, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(base) + off); }
+
+// ---- dispatch (arguments already validated) ----
+int do_route(const moe_shape_t* s, const void* x, const void* w_router, const float* bias, int32_t* topk_idx,
+             float* topk_w, float* keys_out, float* logits, hipStream_t st) {
+  moe::GemmProblem g{};
+  g.X = static_cast<const moe::bf16_t*>(x);
+  g.ldx = s->d;
+  g.offsets = nullptr;
+  g.groups = 1;
+  g.rows_single = s->T;
+  g.max_rows = s->T;
+  g.W = static_cast<const moe::bf16_t*>(w_router);
+  g.w_group_stride = 0;
+  g.N = s->E;
+  g.K = s->d;
+  g.Y = logits;
+  g.ldy = s->E;
+  g.epi = moe::EPI_F32;
+  CHECK(hip_status(moe::launch_grouped_gemm(g, st), "router logits launch"));
+  moe::GateProblem q{};
+  q.logits = logits;
+  q.bias = bias;
+  q.T = s->T;
+  q.E = s->E;
+  q.top_k = s->top_k;
+  q.gate = s->gate;
+  q.n_group = s->n_group;
+  q.topk_group = s->topk_group;
+  q.renormalize = s->renormalize;
+  q.routed_scale = s->routed_scale;
+  q.topk_idx = topk_idx;
+  q.topk_w = topk_w;
+  q.keys_out = keys_out;
+  return hip_status(moe::launch_gate(q, st), "gating launch");
+}
+
+int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int32_t* counts, int32_t* offsets,
+               int32_t* row_token, int32_t* slot_row, void* x_perm, void* ws, hipStream_t st) {
+  moe::PermuteProblem p{};
+  p.topk_idx = topk_idx;
+  p.x = static_cast<const moe::bf16_t*>(x);
+  p.T = s->T;
+  p.d = s->d;
+  p.top_k = s->top_k;
+  p.e_begin = s->e_begin;
+  p.E_local = s->E_local;
+  p.counts = counts;
+  p.offsets = offsets;
+  p.row_token = row_token;
+  p.slot_row = slot_row;
+  p.x_perm = static_cast<moe::bf16_t*>(x_perm);
+  p.cap = capacity(s);
+  p.blk_count = static_cast<int32_t*>(ws);
+  p.blk_base = at<int32_t>(ws, ws_permute(s) / 2);
+  return hip_status(moe::launch_permute(p, st), "permute launch");
+}
+
+int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
+           int d, int F, void* act, void* y, hipStream_t st) {
+  moe::GemmProblem up{};
+  up.X = static_cast<const moe::bf16_t*>(X);
+  up.ldx = d;
+  up.offsets = offsets;
+  up.groups = groups;
+  up.rows_single = rows;
+  up.max_rows = rows;
+  up.W = static_cast<const moe::bf16_t*>(w13);
+  up.w_group_stride = (int64_t)2 * F * d;
+  up.N = F;
+  up.K = d;
+  up.Y = act;
+  up.ldy = F;
+  up.epi = moe::EPI_SWIGLU;
+  CHECK(hip_status(moe::launch_grouped_gemm(up, st), "expert up-projection launch"));
+  moe::GemmProblem dn = up;
+  dn.X = static_cast<const moe::bf16_t*>(act);
+  dn.ldx = F;
+  dn.W = static_cast<const moe::bf16_t*>(w2);
+  dn.w_group_stride = (int64_t)d * F;
+  dn.N = d;
+  dn.K = F;
+  dn.Y = y;
+  dn.ldy = d;
+  dn.epi = moe::EPI_BF16;
+  return hip_status(moe::launch_grouped_gemm(dn, st), "expert down-projection launch");
+}
+
+int do_combine(const moe_shape_t* s, const void* y_perm, const int32_t* slot_row, const float* topk_w,
+               const void* shared_y, void* out, hipStream_t st) {
+  moe::CombineProblem c{};
+  c.y_perm = static_cast<const moe::bf16_t*>(y_perm);
+  c.slot_row = slot_row;
+  c.topk_w = topk_w;
+  c.shared_y = static_cast<const moe::bf16_t*>(shared_y);
+  c.out = static_cast<moe::bf16_t*>(out);
+  c.T = s->T;
+  c.cap = capacity(s);
+  c.d = s->d;
+  c.top_k = s->top_k;
+  return hip_status(moe::launch_combine(c, st), "combine launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+const char* moe_status_string(int status) {
+  switch (status) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG: an argument is NULL, misaligned or inconsistent";
+    case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED: the request is outside the kernels' limits";
+    case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE: the workspace is missing or too small";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP: a HIP call or kernel launch failed";
+    default: return "unknown moe_status_t";
+  }
+}
+
+const char* moe_last_error(void) { return g_err.c_str(); }
+
+size_t moe_workspace_size(const moe_shape_t* shape, int kind) {
+  if (check_shape(shape) != MOE_OK) return 0;
+  if (kind < MOE_WS_ROUTE || kind > MOE_WS_LAYER) {
+    fail(MOE_ERR_INVALID_ARG, "workspace kind (%d) unknown", kind);
+    return 0;
+  }
+  size_t n = ws_need(shape, kind);
+  return n ? n : kAlign;
+}
+
+size_t moe_workspace_offset(const moe_shape_t* shape, int region) {
+  if (check_shape(shape) != MOE_OK) return (size_t)-1;
+  if (region < 0 || region >= MOE_REGION_COUNT_) {
+    fail(MOE_ERR_INVALID_ARG, "region (%d) unknown", region);
+    return (size_t)-1;
+  }
+  return layer_layout(shape).region[region];
+}
+
+int moe_route(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias, int32_t* topk_idx,
+              float* topk_w, float* keys_out, void* ws, size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  if (bias && shape->gate != MOE_GATE_SOFTMAX)
+    return fail(MOE_ERR_UNSUPPORTED, "a router bias is only defined for softmax gating");
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(x, 16, "x"));
+  CHECK(check_ptr(w_router, 16, "w_router"));
+  if (bias) CHECK(check_ptr(bias, 4, "bias"));
+  CHECK(check_ptr(topk_idx, 4, "topk_idx"));
+  CHECK(check_ptr(topk_w, 4, "topk_w"));
+  if (keys_out) CHECK(check_ptr(keys_out, 4, "keys_out"));
+  CHECK(check_ws(shape, MOE_WS_ROUTE, ws, ws_bytes));
+  CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, keys_out, static_cast<float*>(ws), as_stream(stream)));
+  return ok();
+}
+
+int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x, int32_t* counts, int32_t* offsets,
+                int32_t* row_token, int32_t* slot_row, void* x_perm, void* ws, size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(topk_idx, 4, "topk_idx"));
+  CHECK(check_ptr(x, 16, "x"));
+  CHECK(check_ptr(counts, 4, "counts"));
+  CHECK(check_ptr(offsets, 4, "offsets"));
+  CHECK(check_ptr(row_token, 4, "row_token"));
+  CHECK(check_ptr(slot_row, 4, "slot_row"));
+  CHECK(check_ptr(x_perm, 16, "x_perm"));
+  CHECK(check_ws(shape, MOE_WS_PERMUTE, ws, ws_bytes));
+  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, ws, as_stream(stream)));
+  return ok();
+}
+
+int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets, const void* w13,
+                    const void* w2, void* y_perm, void* ws, size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  if (shape->E_local > moe::kMaxGroups)
+    return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", shape->E_local, moe::kMaxGroups);
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(x_perm, 16, "x_perm"));
+  CHECK(check_ptr(offsets, 4, "offsets"));
+  CHECK(check_ptr(w13, 16, "w13"));
+  CHECK(check_ptr(w2, 16, "w2"));
+  CHECK(check_ptr(y_perm, 16, "y_perm"));
+  CHECK(check_ws(shape, MOE_WS_FFN, ws, ws_bytes));
+  CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, ws, y_perm,
+               as_stream(stream)));
+  return ok();
+}
+
+int moe_combine(const moe_shape_t* shape, const void* y_perm, const int32_t* slot_row, const float* topk_w,
+                const void* shared_y, void* out, void* stream) {
+  CHECK(check_shape(shape));
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(y_perm, 16, "y_perm"));
+  CHECK(check_ptr(slot_row, 4, "slot_row"));
+  CHECK(check_ptr(topk_w, 4, "topk_w"));
+  if (shared_y) CHECK(check_ptr(shared_y, 16, "shared_y"));
+  CHECK(check_ptr(out, 16, "out"));
+  CHECK(do_combine(shape, y_perm, slot_row, topk_w, shared_y, out, as_stream(stream)));
+  return ok();
+}
+
+int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                      const void* w13, const void* w2, const void* ws13, const void* ws2, void* out, void* ws,
+                      size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  if (shape->E_local > moe::kMaxGroups)
+    return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", shape->E_local, moe::kMaxGroups);
+  if (bias && shape->gate != MOE_GATE_SOFTMAX)
+    return fail(MOE_ERR_UNSUPPORTED, "a router bias is only defined for softmax gating");
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(x, 16, "x"));
+  CHECK(check_ptr(w_router, 16, "w_router"));
+  if (bias) CHECK(check_ptr(bias, 4, "bias"));
+  CHECK(check_ptr(w13, 16, "w13"));
+  CHECK(check_ptr(w2, 16, "w2"));
+  if (shape->F_shared > 0) {
+    CHECK(check_ptr(ws13, 16, "ws13"));
+    CHECK(check_ptr(ws2, 16, "ws2"));
+  }
+  CHECK(check_ptr(out, 16, "out"));
+  CHECK(check_ws(shape, MOE_WS_LAYER, ws, ws_bytes));
+
+  const LayerLayout L = layer_layout(shape);
+  hipStream_t st = as_stream(stream);
+  int32_t* topk_idx = at<int32_t>(ws, L.region[MOE_REGION_TOPK_IDX]);
+  float* topk_w = at<float>(ws, L.region[MOE_REGION_TOPK_W]);
+  int32_t* counts = at<int32_t>(ws, L.region[MOE_REGION_COUNTS]);
+  int32_t* offsets = at<int32_t>(ws, L.region[MOE_REGION_OFFSETS]);
+  int32_t* row_token = at<int32_t>(ws, L.region[MOE_REGION_ROW_TOKEN]);
+  int32_t* slot_row = at<int32_t>(ws, L.region[MOE_REGION_SLOT_ROW]);
+  void* x_perm = at<void>(ws, L.region[MOE_REGION_X_PERM]);
+  void* y_perm = at<void>(ws, L.region[MOE_REGION_Y_PERM]);
+  void* shared_y = shape->F_shared > 0 ? at<void>(ws, L.region[MOE_REGION_SHARED_Y]) : nullptr;
+
+  CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, nullptr, at<float>(ws, L.logits), st));
+  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, at<void>(ws, L.perm_ws), st));
+  CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, at<void>(ws, L.act),
+               y_perm, st));
+  if (shape->F_shared > 0)
+    CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,
+                 st));
+  CHECK(do_combine(shape, y_perm, slot_row, topk_w, shared_y, out, st));
+  return ok();
+}
+
+}  // extern "C"

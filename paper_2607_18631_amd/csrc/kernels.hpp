@@ -1,0 +1,77 @@
+// Host-side launchers of the gfx950 kernels (internal to libmoe_mi355x.so).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef uint16_t bf16_t;
+
+constexpr int kMaxGroups = 1024;  // E_local limit of the grouped GEMM's in-LDS tile table
+
+enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2 };
+
+// One grouped GEMM  Y[r, n] = sum_k X[r, k] * W_g[n, k]  for every group g and every
+// row r in [offsets[g], offsets[g+1]).  Both operands are K-contiguous.
+// EPI_SWIGLU: W_g holds 2N rows (gate rows [0,N), up rows [N,2N)) and
+//             Y[r, n] = bf16(silu(gate) * up).
+struct GemmProblem {
+  const bf16_t* X;            // token rows, row stride ldx (elements)
+  int64_t ldx;
+  const int32_t* offsets;     // device [groups+1]; nullptr = one group of rows_single rows
+  int32_t groups;
+  int64_t rows_single;
+  int64_t max_rows;           // host-known bound of offsets[groups] (grid sizing only)
+  const bf16_t* W;            // weights of group 0, row stride K
+  int64_t w_group_stride;     // elements between consecutive groups' weights
+  int32_t N;                  // output columns
+  int32_t K;
+  void* Y;                    // bf16 or f32 output, row stride ldy (elements)
+  int64_t ldy;
+  int32_t epi;
+};
+
+hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
+
+struct GateProblem {
+  const float* logits;        // [T, E]
+  const float* bias;          // [E] or nullptr
+  int64_t T;
+  int32_t E, top_k, gate, n_group, topk_group, renormalize;
+  float routed_scale;
+  int32_t* topk_idx;          // [T, top_k]
+  float* topk_w;              // [T, top_k]
+  float* keys_out;            // [T, E] or nullptr
+};
+hipError_t launch_gate(const GateProblem& p, hipStream_t stream);
+
+struct PermuteProblem {
+  const int32_t* topk_idx;    // [T, top_k]
+  const bf16_t* x;            // [T, d]
+  int64_t T;
+  int32_t d, top_k, e_begin, E_local;
+  int32_t* counts;            // [E_local]
+  int32_t* offsets;           // [E_local + 1]
+  int32_t* row_token;         // [cap]
+  int32_t* slot_row;          // [T, top_k]
+  bf16_t* x_perm;             // [cap, d]
+  int64_t cap;                // rows of row_token / x_perm
+  int32_t* blk_count;         // workspace [nblk, E_local]
+  int32_t* blk_base;          // workspace [nblk, E_local]
+};
+int64_t permute_blocks(int64_t T);
+hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream);
+
+struct CombineProblem {
+  const bf16_t* y_perm;       // [cap, d]
+  const int32_t* slot_row;    // [T, top_k]
+  const float* topk_w;        // [T, top_k]
+  const bf16_t* shared_y;     // [T, d] or nullptr
+  bf16_t* out;                // [T, d]
+  int64_t T;
+  int64_t cap;                // rows of y_perm; slot rows outside [0, cap) are skipped
+  int32_t d, top_k;
+};
+hipError_t launch_combine(const CombineProblem& p, hipStream_t stream);
+
+}  // namespace moe

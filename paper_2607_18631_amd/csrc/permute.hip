@@ -1,0 +1,219 @@
+// Histogram, prefix scan and stable permutation of the local (token, expert) slots.
+//
+// Tokens are cut into chunks of 64 (one wavefront).  Three launches:
+//   k_chunk_count  per chunk, how many of its slots go to each local expert
+//   k_chunk_scan   per expert, exclusive scan of the chunk counts over chunks, and
+//                  the expert total (counts[e])
+//   k_permute      per chunk: the offsets (exclusive scan of counts, the monotone
+//                  [E_local+1] array), each slot's rank among the chunk's earlier slots
+//                  of the same expert, hence its row
+//                      row = offsets[e] + chunk_base[c][e] + rank,
+//                  then row_token / slot_row, and the bit-exact copy of every token row
+//                  to each of its local rows (the token is read once, written k_local
+//                  times, 16-byte vectors).
+//
+// The in-chunk rank uses wavefront ballots instead of atomics, so the order inside an
+// expert is ascending token (a stable counting sort) and run-to-run identical: for every
+// slot column j' and every bit b of the local expert id, one ballot gives the lanes whose
+// slot j' has bit b set; AND-ing the matching ballots (or their complements) yields the
+// lanes whose slot j' holds exactly my expert, and the popcount below my lane is the rank.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace moe {
+namespace {
+
+constexpr int CH = 64;          // tokens per chunk = lanes of one wave
+constexpr int kSub = 4;         // copy workgroups per chunk
+
+__global__ __launch_bounds__(64) void k_chunk_count(PermuteProblem p) {
+  extern __shared__ int s_cnt[];   // [E_local]
+  const int lane = threadIdx.x;
+  for (int e = lane; e < p.E_local; e += 64) s_cnt[e] = 0;
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * CH + lane;
+  if (t < p.T) {
+    for (int j = 0; j < p.top_k; ++j) {
+      const int le = p.topk_idx[t * p.top_k + j] - p.e_begin;
+      if (le >= 0 && le < p.E_local) atomicAdd(&s_cnt[le], 1);
+    }
+  }
+  __syncthreads();
+  int32_t* dst = p.blk_count + (int64_t)blockIdx.x * p.E_local;
+  for (int e = lane; e < p.E_local; e += 64) dst[e] = s_cnt[e];
+}
+
+// one workgroup per local expert: exclusive scan of blk_count[:, e] over chunks
+__global__ __launch_bounds__(256) void k_chunk_scan(PermuteProblem p, int nblk) {
+  __shared__ int s_w[4];
+  const int e = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int carry = 0;
+  for (int b0 = 0; b0 < nblk; b0 += 256) {
+    const int b = b0 + tid;
+    const int v = b < nblk ? p.blk_count[(int64_t)b * p.E_local + e] : 0;
+    int inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int n = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += n;
+    }
+    if (lane == 63) s_w[wave] = inc;
+    __syncthreads();
+    int wbase = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (w < wave) wbase += s_w[w];
+      tot += s_w[w];
+    }
+    if (b < nblk) p.blk_base[(int64_t)b * p.E_local + e] = carry + wbase + inc - v;
+    carry += tot;
+    __syncthreads();
+  }
+  if (tid == 0) p.counts[e] = carry;
+}
+
+// grid (nblk, kSub): workgroup (c, s) ranks chunk c and copies its s-th quarter of tokens
+__global__ __launch_bounds__(256) void k_permute(PermuteProblem p) {
+  extern __shared__ int s_dyn[];
+  int* s_off = s_dyn;                          // [E_local + 1]
+  int* s_row = s_dyn + p.E_local + 1;          // [CH * top_k]
+  __shared__ int s_w[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x, sub = blockIdx.y;
+  const int E_local = p.E_local, k = p.top_k;
+
+  // offsets = exclusive scan of counts (every workgroup; workgroup (0,0) publishes it)
+  {
+    constexpr int PER = 4;                     // 256 threads x 4 >= 1024 experts
+    int v[PER], lsum = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = tid * PER + i;
+      v[i] = e < E_local ? p.counts[e] : 0;
+      lsum += v[i];
+    }
+    int inc = lsum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int n = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += n;
+    }
+    if (lane == 63) s_w[wave] = inc;
+    __syncthreads();
+    int run = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (w < wave) run += s_w[w];
+      tot += s_w[w];
+    }
+    run += inc - lsum;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = tid * PER + i;
+      if (e < E_local) s_off[e] = run;
+      run += v[i];
+    }
+    if (tid == 0) s_off[E_local] = tot;
+    __syncthreads();
+    if (c == 0 && sub == 0)
+      for (int e = tid; e <= E_local; e += 256) p.offsets[e] = s_off[e];
+  }
+
+  // rank of each slot inside the chunk (wave 0), rows to LDS
+  const int64_t t0 = (int64_t)c * CH;
+  if (wave == 0) {
+    const int64_t t = t0 + lane;
+    const bool valid_t = t < p.T;
+    int nbits = 0;
+    while ((1 << nbits) < E_local) ++nbits;
+    const int32_t* base = p.blk_base + (int64_t)c * E_local;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int myle[16];
+    int rank[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      myle[j] = -1;
+      rank[j] = 0;
+      if (j < k && valid_t) {
+        const int le = p.topk_idx[t * k + j] - p.e_begin;
+        myle[j] = (le >= 0 && le < E_local) ? le : -1;
+      }
+    }
+#pragma unroll
+    for (int jp = 0; jp < 16; ++jp) {
+      if (jp >= k) break;
+      // lanes whose slot jp is local, and per bit the lanes whose slot jp has that bit set
+      const int lej = myle[jp];
+      const uint64_t vmask = __ballot(lej >= 0);
+      uint64_t bal[10];
+#pragma unroll
+      for (int b = 0; b < 10; ++b) bal[b] = (b < nbits) ? __ballot(lej >= 0 && ((lej >> b) & 1)) : 0ull;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if (j >= k) break;
+        const int le = myle[j];
+        uint64_t m = vmask;
+#pragma unroll
+        for (int b = 0; b < 10; ++b)
+          if (b < nbits) m &= ((le >> b) & 1) ? bal[b] : ~bal[b];
+        rank[j] += __popcll(m & below);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (j >= k) break;
+      int row = -1;
+      if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[j];
+      if (row >= p.cap) row = -1;            // unreachable for a consistent histogram; keeps writes in bounds
+      s_row[lane * k + j] = row;
+      if (sub == 0 && valid_t) {
+        p.slot_row[t * k + j] = row;
+        if (row >= 0) p.row_token[row] = (int32_t)t;
+      }
+    }
+  }
+  __syncthreads();
+
+  // copy: each wave takes tokens of this workgroup's quarter; 16-byte vectors
+  const int per_sub = CH / kSub;
+  const int nvec = p.d / 8;
+  for (int i = wave; i < per_sub; i += 4) {
+    const int l = sub * per_sub + i;
+    const int64_t t = t0 + l;
+    if (t >= p.T) break;
+    int rows[16];
+    bool any = false;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      rows[j] = (j < k) ? s_row[l * k + j] : -1;
+      any |= rows[j] >= 0;
+    }
+    if (!any) continue;
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.x + t * p.d);
+    for (int v = lane; v < nvec; v += 64) {
+      const u32x4 val = src[v];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        if (rows[j] >= 0) reinterpret_cast<u32x4*>(p.x_perm + (int64_t)rows[j] * p.d)[v] = val;
+    }
+  }
+}
+
+}  // namespace
+
+int64_t permute_blocks(int64_t T) { return (T + CH - 1) / CH; }
+
+hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream) {
+  const int64_t nblk = permute_blocks(p.T);
+  hipLaunchKernelGGL(k_chunk_count, dim3((unsigned)nblk), dim3(64), p.E_local * sizeof(int), stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_chunk_scan, dim3((unsigned)p.E_local), dim3(256), 0, stream, p, (int)nblk);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds = (size_t)(p.E_local + 1 + CH * p.top_k) * sizeof(int);
+  hipLaunchKernelGGL(k_permute, dim3((unsigned)nblk, kSub), dim3(256), lds, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace moe

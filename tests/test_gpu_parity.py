@@ -1,0 +1,235 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Small cases compare every output and every intermediate; the five full-size workloads
+run moe_layer_forward in the launch configuration the benchmark times and compare
+routing, counts, offsets and the permutation on all tokens and the layer output on
+sampled tokens.  Edge cases: ragged and single-token batches, non-tile-multiple d and F,
+zero-token experts, one hot expert, a rank slice in the middle of the experts, E = 1024
+with top-16, E = 1 with top-1 (a dense SwiGLU MLP), T = 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_18631_amd import moe
+from paper_2607_18631_amd import workloads as wl
+
+from parity_util import (REL_TOL, check_routing, dev_bits, oracle_routing_with_gpu_ties, rel_fro,
+                         run_route)
+
+pytestmark = pytest.mark.gpu
+
+S = wl.MoEShape
+SMALL = {
+    "tiny": (wl.WORKLOADS["tiny"].shape, 0.02, 0.0),
+    "tiny_T257": (wl.WORKLOADS["tiny"].shape.replace(T=257), 0.02, 0.0),
+    "tiny_T1": (wl.WORKLOADS["tiny"].shape.replace(T=1), 0.02, 0.0),
+    "group_limited_slice": (S(T=300, d=520, E=64, top_k=8, F=1000, E_local=8, e_begin=8, F_shared=264,
+                              gate=wl.GATE_SIGMOID, n_group=8, topk_group=4, routed_scale=2.5), None, 0.0),
+    "skewed_small": (S(T=1000, d=256, E=32, top_k=8, F=96, E_local=32), 2 * 256 ** -0.5, 1.2),
+    "decode_small": (S(T=5, d=1024, E=96, top_k=8, F=256, E_local=12, F_shared=256, gate=wl.GATE_SIGMOID),
+                     None, 0.0),
+    "dense_identity": (S(T=130, d=136, E=1, top_k=1, F=72, E_local=1), None, 0.0),
+    "softmax_no_renorm": (S(T=200, d=128, E=16, top_k=4, F=64, E_local=16, renormalize=0, routed_scale=1.5),
+                          None, 0.0),
+    "sigmoid_slice_end": (S(T=150, d=64, E=40, top_k=5, F=40, E_local=7, e_begin=33, gate=wl.GATE_SIGMOID,
+                            renormalize=0), None, 0.0),
+    "max_experts_top16": (S(T=70, d=64, E=1024, top_k=16, F=16, E_local=1024), None, 0.0),
+}
+
+
+def _inputs(name):
+    sh, rstd, zipf = SMALL[name]
+    return wl.custom_inputs(sh, seed=11, router_std=rstd, zipf_s=zipf)
+
+
+def _intermediates(layer):
+    sh = layer.shape
+    T, k, cap = sh.T, sh.top_k, sh.capacity
+    g = lambda r, dt, shp: layer.region(r, dt, shp).cpu().numpy()
+    return {
+        "topk_idx": g(moe.MOE_REGION_TOPK_IDX, torch.int32, (T, k)),
+        "topk_w": g(moe.MOE_REGION_TOPK_W, torch.float32, (T, k)),
+        "counts": g(moe.MOE_REGION_COUNTS, torch.int32, (sh.E_local,)),
+        "offsets": g(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)),
+        "row_token": g(moe.MOE_REGION_ROW_TOKEN, torch.int32, (cap,)),
+        "slot_row": g(moe.MOE_REGION_SLOT_ROW, torch.int32, (T, k)),
+    }
+
+
+def _check_permutation(sh, inter, g_idx):
+    counts, offsets = oracle.counts_offsets(g_idx, sh.e_begin, sh.E_local)
+    row_token, slot_row = oracle.permutation(g_idx, sh.e_begin, sh.E_local)
+    np.testing.assert_array_equal(inter["topk_idx"], g_idx)
+    np.testing.assert_array_equal(inter["counts"], counts)
+    np.testing.assert_array_equal(inter["offsets"], offsets)
+    n = int(offsets[-1])
+    np.testing.assert_array_equal(inter["row_token"][:n], row_token)
+    np.testing.assert_array_equal(inter["slot_row"], slot_row)
+    return n
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_layer_parity(name):
+    inputs = _inputs(name)
+    sh = inputs["shape"]
+    print(f"[parity] small case {name}: {sh}", flush=True)
+    layer = moe.DeviceLayer(inputs)
+    out = layer.forward()
+    torch.cuda.synchronize()
+    g_idx, g_w, g_keys = run_route(layer)
+    o_idx, o_w, keys64, near = check_routing(inputs, g_idx, g_w, g_keys)
+    inter = _intermediates(layer)
+    np.testing.assert_array_equal(inter["topk_w"], g_w)
+    n = _check_permutation(sh, inter, g_idx)
+    # x_perm rows are bit-exact copies
+    x_perm = dev_bits(layer.region(moe.MOE_REGION_X_PERM, torch.bfloat16, (sh.capacity, sh.d)))
+    np.testing.assert_array_equal(x_perm[:n], inputs["x"][inter["row_token"][:n]])
+    # per-expert MLP rows
+    y_perm = oracle.bf16_to_f64(dev_bits(layer.region(moe.MOE_REGION_Y_PERM, torch.bfloat16,
+                                                       (sh.capacity, sh.d))))
+    xd = oracle.bf16_to_f64(inputs["x"])
+    offs = inter["offsets"]
+    for e in range(sh.E_local):
+        a, b = offs[e], offs[e + 1]
+        if b > a:
+            ref = oracle.swiglu_ffn(xd[inter["row_token"][a:b]], oracle.bf16_to_f64(inputs["w13"][e]),
+                                    oracle.bf16_to_f64(inputs["w2"][e]))
+            assert rel_fro(y_perm[a:b], ref) <= REL_TOL, (e, rel_fro(y_perm[a:b], ref))
+    # layer output
+    idx, w = oracle_routing_with_gpu_ties(o_idx, o_w, keys64, g_idx, near, sh)
+    ref = oracle.expert_outputs_for_tokens(xd, idx, w, sh, inputs["w13"], inputs["w2"], inputs.get("ws13"),
+                                           inputs.get("ws2"))
+    got = oracle.bf16_to_f64(dev_bits(out))
+    err = rel_fro(got, ref)
+    print(f"[parity] {name}: rel_fro={err:.3e} near_ties={len(near)} local_rows={n}", flush=True)
+    assert err <= REL_TOL
+
+
+@pytest.mark.parametrize("name", ["tiny_T257", "group_limited_slice", "decode_small"])
+def test_components_compose_to_layer(name):
+    """route -> permute -> grouped_ffn (+ shared as one group over x) -> combine == layer, bit for bit."""
+    inputs = _inputs(name)
+    sh = inputs["shape"]
+    layer = moe.DeviceLayer(inputs)
+    ref = layer.forward().clone()
+    dev = "cuda"
+    T, k, cap = sh.T, sh.top_k, sh.capacity
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    moe.moe_route(sh, layer.x, layer.w_router, layer.bias, idx, w, None,
+                  moe.alloc_workspace(sh, moe.MOE_WS_ROUTE))
+    counts = torch.empty(sh.E_local, dtype=torch.int32, device=dev)
+    offsets = torch.empty(sh.E_local + 1, dtype=torch.int32, device=dev)
+    row_token = torch.empty(cap, dtype=torch.int32, device=dev)
+    slot_row = torch.empty((T, k), dtype=torch.int32, device=dev)
+    x_perm = torch.empty((cap, sh.d), dtype=torch.bfloat16, device=dev)
+    moe.moe_permute(sh, idx, layer.x, counts, offsets, row_token, slot_row, x_perm,
+                    moe.alloc_workspace(sh, moe.MOE_WS_PERMUTE))
+    y_perm = torch.empty((cap, sh.d), dtype=torch.bfloat16, device=dev)
+    moe.moe_grouped_ffn(sh, x_perm, offsets, layer.w13, layer.w2, y_perm, moe.alloc_workspace(sh, moe.MOE_WS_FFN))
+    shared_y = None
+    if sh.F_shared:
+        ssh = sh.replace(E=1, top_k=1, e_begin=0, E_local=1, F=sh.F_shared, F_shared=0, n_group=1, topk_group=1)
+        soff = torch.tensor([0, T], dtype=torch.int32, device=dev)
+        shared_y = torch.empty((T, sh.d), dtype=torch.bfloat16, device=dev)
+        moe.moe_grouped_ffn(ssh, layer.x, soff, layer.ws13, layer.ws2, shared_y,
+                            moe.alloc_workspace(ssh, moe.MOE_WS_FFN))
+    out = torch.empty((T, sh.d), dtype=torch.bfloat16, device=dev)
+    moe.moe_combine(sh, y_perm, slot_row, w, shared_y, out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dev_bits(out), dev_bits(ref))
+
+
+def test_metamorphic_determinism_scaling_and_token_order():
+    inputs = _inputs("group_limited_slice")
+    sh = inputs["shape"]
+    layer = moe.DeviceLayer(inputs)
+    a = dev_bits(layer.forward().clone())
+    b = dev_bits(layer.forward().clone())
+    np.testing.assert_array_equal(a, b)                           # run to run
+    # doubling W2 and the shared W2 doubles every output exactly
+    layer.w2.mul_(2)
+    layer.ws2.mul_(2)
+    c = oracle.bf16_to_f64(dev_bits(layer.forward().clone()))
+    np.testing.assert_array_equal(c, 2 * oracle.bf16_to_f64(a))
+    # permuting tokens permutes output rows bit for bit
+    perm = np.random.default_rng(0).permutation(sh.T)
+    inp2 = dict(inputs, x=inputs["x"][perm])
+    layer2 = moe.DeviceLayer(inp2)
+    d = dev_bits(layer2.forward())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(d, a[perm])
+
+
+def test_expert_relabel_invariance():
+    inputs = _inputs("skewed_small")
+    sh = inputs["shape"]
+    a = dev_bits(moe.DeviceLayer(inputs).forward())
+    pi = np.random.default_rng(1).permutation(sh.E)                # new id of old expert e is pi[e]
+    inv = np.argsort(pi)
+    inp2 = dict(inputs, w_router=inputs["w_router"][inv], bias=inputs["bias"][inv], w13=inputs["w13"][inv],
+                w2=inputs["w2"][inv])
+    b = dev_bits(moe.DeviceLayer(inp2).forward())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(a, b)
+
+
+def test_single_hot_expert():
+    sh = S(T=700, d=192, E=8, top_k=2, F=128, E_local=8)
+    inputs = wl.custom_inputs(sh, seed=5)
+    bias = np.zeros(8, np.float32)
+    bias[3] = 40.0                                                 # every token picks expert 3 first
+    inputs["bias"] = bias
+    layer = moe.DeviceLayer(inputs)
+    out = layer.forward()
+    torch.cuda.synchronize()
+    inter = _intermediates(layer)
+    assert inter["counts"][3] == sh.T and (inter["topk_idx"][:, 0] == 3).all()
+    g_idx, g_w, g_keys = run_route(layer)
+    o_idx, o_w, keys64, near = check_routing(inputs, g_idx, g_w, g_keys)
+    _check_permutation(sh, inter, g_idx)
+    idx, w = oracle_routing_with_gpu_ties(o_idx, o_w, keys64, g_idx, near, sh)
+    ref = oracle.expert_outputs_for_tokens(oracle.bf16_to_f64(inputs["x"]), idx, w, sh, inputs["w13"],
+                                           inputs["w2"])
+    assert rel_fro(oracle.bf16_to_f64(dev_bits(out)), ref) <= REL_TOL
+
+
+def test_zero_tokens_noop_on_device():
+    sh = wl.WORKLOADS["tiny"].shape.replace(T=0)
+    moe.moe_layer_forward(sh, None, None, None, None, None, None, None, None, None)
+
+
+# ---------------------------------------------------------------------------------------
+# full-size workloads, launch configuration of the benchmark
+# ---------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name", list(wl.WORKLOADS))
+def test_full_workload_parity(name):
+    print(f"[parity] full workload {name}: generating inputs", flush=True)
+    inputs = wl.make_inputs(name)
+    sh = inputs["shape"]
+    layer = moe.DeviceLayer(inputs)
+    out = layer.forward()
+    torch.cuda.synchronize()
+    print(f"[parity] {name}: layer ran, checking routing on {sh.T} tokens", flush=True)
+    g_idx, g_w, g_keys = run_route(layer)
+    xd = oracle.bf16_to_f64(inputs["x"])
+    o_idx, o_w, keys64, near = check_routing(inputs, g_idx, g_w, g_keys, xd)
+    inter = _intermediates(layer)
+    np.testing.assert_array_equal(inter["topk_w"], g_w)
+    n = _check_permutation(sh, inter, g_idx)
+    x_perm = dev_bits(layer.region(moe.MOE_REGION_X_PERM, torch.bfloat16, (sh.capacity, sh.d))[:n])
+    np.testing.assert_array_equal(x_perm, inputs["x"][inter["row_token"][:n]])
+    # sampled output rows (plus every near-tie token)
+    rng = np.random.default_rng(123)
+    toks = np.unique(np.concatenate([rng.choice(sh.T, size=min(sh.T, 48), replace=False), np.array(near, int)]))
+    idx, w = oracle_routing_with_gpu_ties(o_idx, o_w, keys64, g_idx, near, sh)
+    ref = oracle.expert_outputs_for_tokens(xd[toks], idx[toks], w[toks], sh, inputs["w13"], inputs["w2"],
+                                           inputs.get("ws13"), inputs.get("ws2"))
+    got = oracle.bf16_to_f64(dev_bits(out)[toks])
+    err = rel_fro(got, ref)
+    cnt = inter["counts"]
+    print(f"[parity] {name}: rel_fro={err:.3e} on {toks.size} tokens, near_ties={len(near)}, local rows={n}, "
+          f"counts min/median/max={cnt.min()}/{int(np.median(cnt))}/{cnt.max()}", flush=True)
+    assert err <= REL_TOL
