@@ -1,0 +1,211 @@
+"""Benchmark of the MoE-layer forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload dsv3] [--no-cpu-baseline]
+
+One step = one moe_layer_forward (router logits, gating/top-k, histogram + scan,
+permutation, grouped SwiGLU expert MLP, shared expert, combine) over one batch of
+seeded synthetic input already resident in HBM.  Prints ONE JSON line.
+
+Default workload: the DeepSeek-V3-shaped rank share (T=8192, d=7168, 256 routed experts,
+top-8 sigmoid gating with 8 groups / top-4 groups, 32 local experts of width 2048 plus
+one shared expert of width 2048), the configuration the grouped-GEMM and HBM targets
+are quoted on.
+
+The dominant kernel's roofline figure uses per-step HIP events recorded by
+moe_layer_forward_traced inside the timed region; the CPU baseline times the fp64 oracle
+on a bounded sample of the same batch on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime's C API (timing events)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            h = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            arr[i] = h
+        return arr
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, arr):
+        for h in arr:
+            self.hip.hipEventDestroy(h)
+
+
+def gating_desc(sh):
+    g = "softmax" if sh.gate == 0 else "sigmoid"
+    if sh.n_group > 1:
+        g += f", {sh.n_group} groups / top-{sh.topk_group}"
+    g += ", renormalised" if sh.renormalize else ""
+    if sh.routed_scale != 1.0:
+        g += f" x{sh.routed_scale:g}"
+    return g
+
+
+def cpu_baseline(inputs, sample_tokens):
+    """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
+    import numpy as np
+
+    import oracle
+    sh = inputs["shape"]
+    n = min(sample_tokens, sh.T)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    xd = oracle.bf16_to_f64(inputs["x"][:n])
+    idx, w, _ = oracle.route(xd, oracle.bf16_to_f64(inputs["w_router"]), sh, inputs.get("bias"))
+    out = oracle.expert_outputs_for_tokens(xd, idx, w, sh, inputs["w13"], inputs["w2"], inputs.get("ws13"),
+                                           inputs.get("ws2"))
+    dt = time.perf_counter() - t0
+    assert np.isfinite(out).all()
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} of {sh.T} tokens of the same batch: fp64 routing, expert and shared SwiGLU "
+                      f"MLPs and combine ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dsv3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=8192, help="tokens of the oracle CPU baseline sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs the MoE-layer forward of one expert-parallel rank on ONE GPU; "
+                                   "--gpus must be 1 (multi-GPU sharding is described, not built)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    log(f"generating inputs of workload {args.workload}")
+    inputs = wl.make_inputs(args.workload)
+    sh = inputs["shape"]
+    layer = moe.DeviceLayer(inputs, device="cuda:0")
+    torch.cuda.synchronize()
+    ev = HipEvents()
+    nstep = len(moe.MOE_STEP_NAMES)
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        layer.forward()
+    torch.cuda.synchronize()
+
+    events = [ev.create(nstep + 1) for _ in range(args.steps)]
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        layer.forward_traced(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in events])  # ms
+    gpu_total = sum(ev.elapsed_ms(e[0], e[nstep]) for e in events)
+    for e in events:
+        ev.destroy(e)
+    ms_step = wall * 1e3 / args.steps
+
+    # algorithmic work of this batch (from the routing the GPU produced)
+    offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
+    slot_row = layer.region(moe.MOE_REGION_SLOT_ROW, torch.int32, (sh.T, sh.top_k)).cpu().numpy()
+    out = layer.out.float()
+    assert bool(torch.isfinite(out).all()), "non-finite layer output"
+    n_loc = int(offsets[-1])
+    tok_local = int((slot_row >= 0).any(axis=1).sum())
+    d, F, Fs, T, k = sh.d, sh.F, sh.F_shared, sh.T, sh.top_k
+    up_flops = 4.0 * d * F * n_loc + 4.0 * d * Fs * T
+    gemm_flops = 6.0 * d * F * n_loc + 6.0 * d * Fs * T
+    med = np.median(per_step, axis=0)
+    avg = per_step.mean(axis=0)
+    s = {name: i for i, name in enumerate(moe.MOE_STEP_NAMES)}
+    up_ms = avg[s["ffn_up"]] + avg[s["shared_up"]]
+    up_launches = 2 if Fs > 0 else 1
+    gemm_ms = sum(avg[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
+    perm_bytes = (tok_local + n_loc) * d * 2 + T * k * 8 + n_loc * 4
+    comb_bytes = n_loc * d * 2 + (T * d * 2 if Fs > 0 else 0) + T * d * 2 + T * k * 8
+    achieved = up_flops / (up_ms * 1e-3) / 1e12
+    res = {
+        "metric": "MoE-layer tokens/s + grouped-GEMM TFLOP/s (% bf16 MFMA peak), 1 MI355X",
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "T": T, "d": d, "E": sh.E, "top_k": k, "E_local": sh.E_local,
+                   "e_begin": sh.e_begin, "F": F, "F_shared": Fs, "gating": gating_desc(sh), "seed": inputs["seed"],
+                   "local_rows": n_loc, "parallelism": "one expert-parallel rank's share on 1 GPU"},
+        "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
+        "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "permute_gbs": perm_bytes / (avg[s["permute"]] * 1e-3) / 1e9,
+        "combine_gbs": comb_bytes / (avg[s["combine"]] * 1e-3) / 1e9,
+        "step_ms": {n: round(float(med[i]), 5) for n, i in s.items()},
+        "gpu_event_ms_per_step": gpu_total / args.steps,
+        "roofline": {
+            "kernel": "k_grouped_gemm<EPI_SWIGLU> (expert W1/W3 GEMM + SwiGLU; routed and shared launches)",
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": None,
+            "launches_per_step": up_launches,
+            "avg_launch_ms": float(up_ms / up_launches),
+            "flops_per_step": up_flops,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {args.cpu_sample} tokens")
+        res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_sample)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

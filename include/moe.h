@@ -189,6 +189,29 @@ int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_rou
                       const void* w13, const void* w2, const void* ws13, const void* ws2,
                       void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* Steps of moe_layer_forward, in launch order (moe_layer_forward_traced). */
+typedef enum moe_step {
+  MOE_STEP_ROUTER_GEMM = 0,   /* router logits (grouped GEMM, one group, f32 out)   */
+  MOE_STEP_GATE = 1,          /* gating + top-k                                     */
+  MOE_STEP_HISTOGRAM = 2,     /* per-chunk histogram + scan over chunks             */
+  MOE_STEP_PERMUTE = 3,       /* offsets, stable ranks, row copy                    */
+  MOE_STEP_FFN_UP = 4,        /* routed experts: W1/W3 GEMM + SwiGLU                */
+  MOE_STEP_FFN_DOWN = 5,      /* routed experts: W2 GEMM                            */
+  MOE_STEP_SHARED_UP = 6,     /* shared expert: W1/W3 GEMM + SwiGLU (if F_shared)   */
+  MOE_STEP_SHARED_DOWN = 7,   /* shared expert: W2 GEMM (if F_shared)               */
+  MOE_STEP_COMBINE = 8,       /* gate-weighted combine                              */
+  MOE_STEP_COUNT_ = 9
+} moe_step_t;
+
+/* moe_layer_forward with per-step timing for profilers and benchmarks: `events` holds
+ * MOE_STEP_COUNT_ + 1 hipEvent_t (as opaque pointers) created by the caller; events[i]
+ * is recorded on `stream` right before step i is enqueued and events[MOE_STEP_COUNT_]
+ * after the last step (a step that does not run gets its event recorded all the same,
+ * so its interval is empty).  events == NULL behaves exactly like moe_layer_forward. */
+int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                             const void* w13, const void* w2, const void* ws13, const void* ws2,
+                             void* out, void* ws, size_t ws_bytes, void* const* events, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -156,8 +156,17 @@ template <class T>
 inline T* at(void* base, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(base) + off); }
 
 // ---- dispatch (arguments already validated) ----
+using Marker = int (*)(int step);
+thread_local void* const* g_events = nullptr;
+thread_local hipStream_t g_event_stream = nullptr;
+int mark_event(int step) {
+  return hip_status(hipEventRecord(static_cast<hipEvent_t>(g_events[step]), g_event_stream), "hipEventRecord");
+}
+
+int mark_permute() { return mark_event(MOE_STEP_PERMUTE); }
+
 int do_route(const moe_shape_t* s, const void* x, const void* w_router, const float* bias, int32_t* topk_idx,
-             float* topk_w, float* keys_out, float* logits, hipStream_t st) {
+             float* topk_w, float* keys_out, float* logits, hipStream_t st, Marker mark = nullptr) {
   moe::GemmProblem g{};
   g.X = static_cast<const moe::bf16_t*>(x);
   g.ldx = s->d;
@@ -173,6 +182,7 @@ int do_route(const moe_shape_t* s, const void* x, const void* w_router, const fl
   g.ldy = s->E;
   g.epi = moe::EPI_F32;
   CHECK(hip_status(moe::launch_grouped_gemm(g, st), "router logits launch"));
+  if (mark) CHECK(mark(MOE_STEP_GATE));
   moe::GateProblem q{};
   q.logits = logits;
   q.bias = bias;
@@ -191,7 +201,8 @@ int do_route(const moe_shape_t* s, const void* x, const void* w_router, const fl
 }
 
 int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int32_t* counts, int32_t* offsets,
-               int32_t* row_token, int32_t* slot_row, void* x_perm, void* ws, hipStream_t st) {
+               int32_t* row_token, int32_t* slot_row, void* x_perm, void* ws, hipStream_t st,
+               Marker mark = nullptr) {
   moe::PermuteProblem p{};
   p.topk_idx = topk_idx;
   p.x = static_cast<const moe::bf16_t*>(x);
@@ -208,11 +219,12 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
   p.cap = capacity(s);
   p.blk_count = static_cast<int32_t*>(ws);
   p.blk_base = at<int32_t>(ws, ws_permute(s) / 2);
-  return hip_status(moe::launch_permute(p, st), "permute launch");
+  return hip_status(moe::launch_permute(p, st, mark ? mark_permute : nullptr),
+                    "permute launch");
 }
 
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
-           int d, int F, void* act, void* y, hipStream_t st) {
+           int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0) {
   moe::GemmProblem up{};
   up.X = static_cast<const moe::bf16_t*>(X);
   up.ldx = d;
@@ -228,6 +240,7 @@ int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, cons
   up.ldy = F;
   up.epi = moe::EPI_SWIGLU;
   CHECK(hip_status(moe::launch_grouped_gemm(up, st), "expert up-projection launch"));
+  if (mark) CHECK(mark(down_step));
   moe::GemmProblem dn = up;
   dn.X = static_cast<const moe::bf16_t*>(act);
   dn.ldx = F;
@@ -357,9 +370,9 @@ int moe_combine(const moe_shape_t* shape, const void* y_perm, const int32_t* slo
   return ok();
 }
 
-int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
-                      const void* w13, const void* w2, const void* ws13, const void* ws2, void* out, void* ws,
-                      size_t ws_bytes, void* stream) {
+int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                             const void* w13, const void* w2, const void* ws13, const void* ws2, void* out,
+                             void* ws, size_t ws_bytes, void* const* events, void* stream) {
   CHECK(check_shape(shape));
   if (shape->E_local > moe::kMaxGroups)
     return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", shape->E_local, moe::kMaxGroups);
@@ -377,9 +390,15 @@ int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_rou
   }
   CHECK(check_ptr(out, 16, "out"));
   CHECK(check_ws(shape, MOE_WS_LAYER, ws, ws_bytes));
+  if (events)
+    for (int i = 0; i <= MOE_STEP_COUNT_; ++i)
+      if (!events[i]) return fail(MOE_ERR_INVALID_ARG, "events[%d] is NULL", i);
 
   const LayerLayout L = layer_layout(shape);
   hipStream_t st = as_stream(stream);
+  g_events = events;
+  g_event_stream = st;
+  Marker mark = events ? mark_event : nullptr;
   int32_t* topk_idx = at<int32_t>(ws, L.region[MOE_REGION_TOPK_IDX]);
   float* topk_w = at<float>(ws, L.region[MOE_REGION_TOPK_W]);
   int32_t* counts = at<int32_t>(ws, L.region[MOE_REGION_COUNTS]);
@@ -390,15 +409,32 @@ int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_rou
   void* y_perm = at<void>(ws, L.region[MOE_REGION_Y_PERM]);
   void* shared_y = shape->F_shared > 0 ? at<void>(ws, L.region[MOE_REGION_SHARED_Y]) : nullptr;
 
-  CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, nullptr, at<float>(ws, L.logits), st));
-  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, at<void>(ws, L.perm_ws), st));
+  if (mark) CHECK(mark(MOE_STEP_ROUTER_GEMM));
+  CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, nullptr, at<float>(ws, L.logits), st, mark));
+  if (mark) CHECK(mark(MOE_STEP_HISTOGRAM));
+  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, at<void>(ws, L.perm_ws), st,
+                   mark));
+  if (mark) CHECK(mark(MOE_STEP_FFN_UP));
   CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, at<void>(ws, L.act),
-               y_perm, st));
+               y_perm, st, mark, MOE_STEP_FFN_DOWN));
+  if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
   if (shape->F_shared > 0)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,
-                 st));
+                 st, mark, MOE_STEP_SHARED_DOWN));
+  else if (mark)
+    CHECK(mark(MOE_STEP_SHARED_DOWN));
+  if (mark) CHECK(mark(MOE_STEP_COMBINE));
   CHECK(do_combine(shape, y_perm, slot_row, topk_w, shared_y, out, st));
+  if (mark) CHECK(mark(MOE_STEP_COUNT_));
+  g_events = nullptr;
   return ok();
+}
+
+int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                      const void* w13, const void* w2, const void* ws13, const void* ws2, void* out, void* ws,
+                      size_t ws_bytes, void* stream) {
+  return moe_layer_forward_traced(shape, x, w_router, bias, w13, w2, ws13, ws2, out, ws, ws_bytes, nullptr,
+                                  stream);
 }
 
 }  // extern "C"

@@ -60,7 +60,9 @@ struct PermuteProblem {
   int32_t* blk_base;          // workspace [nblk, E_local]
 };
 int64_t permute_blocks(int64_t T);
-hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream);
+// `between` (may be empty) runs on the host after the histogram launches and before the
+// permute launch (used to record a timing event between the two steps).
+hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*between)() = nullptr);
 
 struct CombineProblem {
   const bf16_t* y_perm;       // [cap, d]

@@ -203,7 +203,7 @@ __global__ __launch_bounds__(256) void k_permute(PermuteProblem p) {
 
 int64_t permute_blocks(int64_t T) { return (T + CH - 1) / CH; }
 
-hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream) {
+hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*between)()) {
   const int64_t nblk = permute_blocks(p.T);
   hipLaunchKernelGGL(k_chunk_count, dim3((unsigned)nblk), dim3(64), p.E_local * sizeof(int), stream, p);
   hipError_t e = hipGetLastError();
@@ -211,6 +211,7 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream) {
   hipLaunchKernelGGL(k_chunk_scan, dim3((unsigned)p.E_local), dim3(256), 0, stream, p, (int)nblk);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (between && between() != 0) return hipErrorUnknown;
   const size_t lds = (size_t)(p.E_local + 1 + CH * p.top_k) * sizeof(int);
   hipLaunchKernelGGL(k_permute, dim3((unsigned)nblk, kSub), dim3(256), lds, stream, p);
   return hipGetLastError();

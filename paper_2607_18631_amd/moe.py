@@ -24,7 +24,9 @@ MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER = range(4)
 
 EXPORTS = ["moe_abi_version", "moe_status_string", "moe_last_error", "moe_workspace_size",
            "moe_workspace_offset", "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
-           "moe_layer_forward"]
+           "moe_layer_forward", "moe_layer_forward_traced"]
+MOE_STEP_NAMES = ["router_gemm", "gate", "histogram", "permute", "ffn_up", "ffn_down", "shared_up",
+                  "shared_down", "combine"]
 
 
 class MoEShapeC(ctypes.Structure):
@@ -66,7 +68,10 @@ def lib():
         L.moe_grouped_ffn.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_combine.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.moe_layer_forward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
-        for f in ("moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine", "moe_layer_forward"):
+        L.moe_layer_forward_traced.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                               ctypes.POINTER(_vp), _vp]
+        for f in ("moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine", "moe_layer_forward",
+                  "moe_layer_forward_traced"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -144,6 +149,13 @@ def moe_layer_forward(sh, x, w_router, bias, w13, w2, ws13, ws2, out, ws, stream
                                    _stream(stream)))
 
 
+def moe_layer_forward_traced(sh, x, w_router, bias, w13, w2, ws13, ws2, out, ws, events, stream=None):
+    """``events``: ctypes array of len(MOE_STEP_NAMES) + 1 hipEvent_t handles (or None)."""
+    _check(lib().moe_layer_forward_traced(ctypes.byref(shape_c(sh)), _p(x), _p(w_router), _p(bias), _p(w13),
+                                          _p(w2), _p(ws13), _p(ws2), _p(out), _p(ws),
+                                          0 if ws is None else ws.numel(), events, _stream(stream)))
+
+
 # ---------------------------------------------------------------------------------------
 # device placement helpers (torch is plumbing: memory and streams)
 # ---------------------------------------------------------------------------------------
@@ -183,6 +195,11 @@ class DeviceLayer:
     def forward(self, stream=None):
         moe_layer_forward(self.shape, self.x, self.w_router, self.bias, self.w13, self.w2, self.ws13, self.ws2,
                           self.out, self.ws, stream)
+        return self.out
+
+    def forward_traced(self, events, stream=None):
+        moe_layer_forward_traced(self.shape, self.x, self.w_router, self.bias, self.w13, self.w2, self.ws13,
+                                 self.ws2, self.out, self.ws, events, stream)
         return self.out
 
     def region(self, region: int, dtype, shape):
