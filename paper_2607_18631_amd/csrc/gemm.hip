@@ -1,40 +1,94 @@
 // Grouped GEMM on gfx950 bf16 MFMA (v_mfma_f32_32x32x16_bf16), fp32 accumulation.
 //
+//   Y[r, n] = sum_k X[r, k] * W_g[n, k]     for every group g, every row r in [offs[g], offs[g+1])
+//
 // One launch serves every group (local expert) of a batch: the row segment of group g
 // is [offsets[g], offsets[g+1]) -- the monotone [E+1] row-offset array of the paper's
-// kernel-generation section -- read from device memory, so the number of rows never
-// travels to the host.  Each workgroup builds the tile table of the launch in LDS
-// (ceil(m_g / BM) x n-tiles per group, a block-wide prefix sum) and then walks tiles
-// persistently.  Tiles of one group are ordered m-fastest so that the tiles sharing a
-// weight tile are adjacent, and adjacent tiles are handed to workgroups of the same
-// XCD (workgroup i runs on XCD i mod 8), so a weight tile is fetched from HBM once per
-// XCD L2 rather than once per m-tile.
+// kernel-generation section -- read from device memory, so the row counts never travel
+// to the host.  Each workgroup builds the launch's tile table in LDS (ceil(m_g / BM) x
+// n-tiles per group, one block-wide prefix sum) and then walks tiles persistently.
+// Tiles of one group are ordered m-fastest, so the m-tiles sharing a weight tile are
+// adjacent, and adjacent tiles go to workgroups of the same XCD (workgroup i runs on XCD
+// i mod 8): a weight tile is fetched from HBM once per XCD L2, not once per m-tile.
+//
+// Data movement: K is consumed in BK-wide slices through a STAGES-deep LDS ring.  Slices
+// are copied global -> LDS by the direct-to-LDS loads of gfx950 (global_load_lds_dwordx4:
+// lane i of a wave instruction writes bytes [16 i, 16 i + 16) after the wave's LDS base),
+// issued STAGES-1 slices ahead, so HBM/L2 latency hides behind the MFMAs of the slices in
+// between and no VGPR staging is needed.  A slice is consumed after `s_waitcnt vmcnt`
+// (this wave's copies of it have landed) and a workgroup barrier (everyone's have).
+// The barrier also orders the reuse of a ring slot: the slot refilled in iteration kt was
+// last read in iteration kt-1, which every wave has finished once it passes the barrier.
+//
+// LDS layout of a slice: [rows][BK] bf16, row r's 16-byte chunk c stored at chunk
+// c ^ f(r), f(r) = (r / (16 / CPR)) % CPR with CPR = BK / 8 chunks per row.  The 16 lanes of
+// one ds_read_b128 phase read one logical chunk of 16 consecutive rows and hit 16
+// distinct 16-byte bank groups.  The swizzle is applied on the global side: a lane
+// fetches the logical chunk that belongs at its fixed LDS position.
 //
 // Operand roles: the weight tile is the MFMA A operand (rows = output features) and the
 // token tile the B operand (columns = tokens), so each lane ends with 4 consecutive
 // output features of one token: 8-byte bf16 stores along the output row.
 //
-// LDS: both tiles are [rows][64] bf16 (128 B per row = 8 chunks of 16 B); chunk c of row r
-// lives at chunk c ^ ((r >> 1) & 7), so the 16 lanes of one ds_read_b128 phase (16
-// consecutive rows, one logical chunk) cover all 64 banks once.  Two stages: while the
-// MFMAs consume stage s, the next K slice is already in registers and is written to
-// stage s^1 afterwards (one barrier per K slice).
+// Edges: token rows past the group's end and weight rows past N are clamped to the last
+// valid row (their results are never stored); a K tail (K % BK != 0) is fetched from
+// clamped addresses and its chunks past K are zeroed in LDS before use.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace moe {
 namespace {
 
-constexpr int BK = 64;
-constexpr int NT = 256;
+#ifndef MOE_BAND_M
+#define MOE_BAND_M 8
+#endif
+constexpr int BAND_M = MOE_BAND_M;   // m-tiles per band of the tile order
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 1) & 7)) << 3); }
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"I"(N) : "memory");
+}
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ void raw_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-__device__ __forceinline__ bf16x8 lds_frag(const bf16_t* tile, int row, int chunk) {
-  return *reinterpret_cast<const bf16x8*>(tile + swz(row, chunk));
+// 16-byte direct-to-LDS copy of one wave instruction: lane i fetches `src` (its own
+// address) into bytes [16 i, 16 i + 16) after the wave-uniform LDS address `dst`.
+__device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
 }
 
-// Block-wide exclusive scan of one int per thread (NT threads); returns the block total.
+// Instruction-scheduler directives for one MFMA K-step: an MFMA first, then the next
+// step's LDS reads two at a time between MFMAs, then the remaining MFMAs.
+template <int REM>
+__device__ __forceinline__ void sched_read_pairs() {
+  if constexpr (REM > 0) {
+    __builtin_amdgcn_sched_group_barrier(0x100, REM >= 2 ? 2 : 1, 0);   // DS read(s)
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA
+    sched_read_pairs<REM - 2>();
+  }
+}
+template <int NR, int NMF>
+__device__ __forceinline__ void sched_step() {
+  if constexpr (NMF >= (NR + 1) / 2 + 1) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    sched_read_pairs<NR>();
+    if constexpr (NMF - (NR + 1) / 2 - 1 > 0)
+      __builtin_amdgcn_sched_group_barrier(0x008, NMF - (NR + 1) / 2 - 1, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int BK>
+struct Swz {
+  static constexpr int CPR = BK / 8;            // 16-byte chunks per row
+  static constexpr int RPG = 16 / CPR;          // rows per 256-byte bank cycle
+  __device__ static __forceinline__ int f(int row) { return (row / RPG) % CPR; }
+  __device__ static __forceinline__ int off(int row, int chunk) { return row * BK + ((chunk ^ f(row)) << 3); }
+};
+
+// Block-wide exclusive scan of one int per thread (NTH threads); returns the block total.
+template <int NTH>
 __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int inc = v;
@@ -47,7 +101,7 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
   __syncthreads();
   int wbase = 0, total = 0;
 #pragma unroll
-  for (int w = 0; w < NT / 64; ++w) {
+  for (int w = 0; w < NTH / 64; ++w) {
     int t = s_tmp[w];
     if (w < wave) wbase += t;
     total += t;
@@ -57,24 +111,34 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
   return total;
 }
 
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
-  constexpr int WM = BM / 2, WN = BN / 2;      // 2 x 2 waves
-  constexpr int FM = WM / 32, FN = WN / 32;    // 32x32 fragments per wave
-  constexpr int XCH = BM * 8 / NT, WCH = BN * 8 / NT;
+// BM token rows x BN weight rows per tile, WGM x WGN waves (each a (BM/WGM) x (BN/WGN)
+// sub-tile), BK-wide K slices through a STAGES-deep ring.
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem p) {
+  using S = Swz<BK>;
+  constexpr int NW = WGM * WGN, NTH = 64 * NW;
+  constexpr int WM = BM / WGM, WN = BN / WGN;             // per-wave sub-tile
+  constexpr int FM = WM / 32, FN = WN / 32;               // 32x32 fragments per wave
+  constexpr int ROWS_PER_INST = 1024 / (BK * 2);          // rows one wave instruction fills
+  constexpr int QX = BM / ROWS_PER_INST, QW = BN / ROWS_PER_INST;   // instructions per slice
+  constexpr int LX = QX / NW, LW = QW / NW;               // ... per wave
+  constexpr int L = LX + LW;                              // vector-memory ops per wave per slice
   constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
-  static_assert(FM >= 1 && FN >= 1 && XCH >= 1 && WCH >= 1, "tile too small");
-  static_assert(EPI != EPI_SWIGLU || FN % 2 == 0, "SwiGLU pairs gate and up fragments");
+  constexpr int HALF_W = (EPI == EPI_SWIGLU) ? BN / 2 / WGN : WN;   // gate rows per wave (SwiGLU)
+  constexpr int SLICE = (BM + BN) * BK;                   // bf16 elements per ring slot
+  static_assert(FM >= 1 && FN >= 1 && QX % NW == 0 && QW % NW == 0, "tile too small");
+  static_assert(EPI != EPI_SWIGLU || (FN % 2 == 0 && HALF_W % 32 == 0), "SwiGLU pairs gate and up fragments");
+  static_assert(STAGES >= 2 && (STAGES - 2) * L < 64, "ring depth");
 
   extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* sX = reinterpret_cast<bf16_t*>(smem);              // [2][BM][BK]
-  bf16_t* sW = sX + 2 * BM * BK;                              // [2][BN][BK]
+  bf16_t* ring = reinterpret_cast<bf16_t*>(smem);         // [STAGES][BM + BN][BK]: X rows then W rows
   __shared__ int s_off[kMaxGroups + 1];
   __shared__ int s_tp[kMaxGroups + 1];
-  __shared__ int s_tmp[NT / 64];
+  __shared__ int s_tmp[NTH / 64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_n = (p.N + OUTN - 1) / OUTN;
 
   // ---- tile table: s_tp[g] = first tile of group g ----
@@ -82,13 +146,13 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
   if (p.offsets) {
     // clamp to [0, max_rows]: any offsets content keeps every access inside the buffers
     const int cap = (int)p.max_rows;
-    for (int g = tid; g <= groups; g += NT) s_off[g] = min(max(p.offsets[g], 0), cap);
+    for (int g = tid; g <= groups; g += NTH) s_off[g] = min(max(p.offsets[g], 0), cap);
   } else {
     groups = 1;
     if (tid == 0) { s_off[0] = 0; s_off[1] = (int)p.rows_single; }
   }
   __syncthreads();
-  constexpr int PER = (kMaxGroups + NT - 1) / NT;
+  constexpr int PER = (kMaxGroups + NTH - 1) / NTH;
   int loc[PER];
   int lsum = 0;
 #pragma unroll
@@ -99,7 +163,7 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
     lsum += loc[i];
   }
   int excl;
-  const int total = block_exclusive_scan(lsum, s_tmp, excl);
+  const int total = block_exclusive_scan<NTH>(lsum, s_tmp, excl);
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     int g = tid * PER + i;
@@ -111,75 +175,174 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
 
   const int G = gridDim.x;
   const int slot = (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+  const int K = p.K;
+  const int nk = (K + BK - 1) / BK;
+  constexpr bool ktail = KTAIL;                           // K % BK != 0 (launcher-checked)
 
-  for (int base = 0; base < total; base += G) {
-    const int tile = base + slot;
-    if (tile >= total) break;
-    // group of this tile: last g with s_tp[g] <= tile
-    int lo = 0, hi = groups;             // s_tp[groups] == total > tile
+  // lane's position inside one wave instruction: row offset and physical chunk
+  const int li_row = lane / S::CPR;                       // 0 .. ROWS_PER_INST-1
+  const int li_pc = lane % S::CPR;
+
+  // weight-row base (inside the W tile) of each fragment of this wave
+  int wbase[FN];
+#pragma unroll
+  for (int b = 0; b < FN; ++b) {
+    if (EPI == EPI_SWIGLU)
+      wbase[b] = (b < FN / 2) ? wn * HALF_W + b * 32 : BN / 2 + wn * HALF_W + (b - FN / 2) * 32;
+    else
+      wbase[b] = wn * WN + b * 32;
+  }
+
+  // Per-tile copy sources: a wave-uniform base (scalar registers) per copy instruction and a
+  // fixed per-lane 32-bit byte offset (row * ld + logical chunk), so a full slice's copies
+  // cost one scalar add each and no vector ALU.  The W instruction j is uniformly in the gate
+  // or the up half of a SwiGLU tile.
+  const char* xbase;
+  const char* wsb[LW];
+  uint32_t xoff[LX], woff[LW];
+  int xchunk[LX], wchunk[LW];
+
+  auto setup_tile = [&](int tile, int& row0, int& row_end, int& ni) {
+    int lo = 0, hi = groups;                              // s_tp[groups] == total > tile
     while (hi - lo > 1) {
       int mid = (lo + hi) >> 1;
       if (s_tp[mid] <= tile) lo = mid; else hi = mid;
     }
-    const int g = lo;
-    const int row0g = s_off[g], row_end = s_off[g + 1];
+    const int g = __builtin_amdgcn_readfirstlane(lo);
+    const int row0g = __builtin_amdgcn_readfirstlane(s_off[g]);
+    row_end = __builtin_amdgcn_readfirstlane(s_off[g + 1]);
     const int mt = (row_end - row0g + BM - 1) / BM;
-    const int local = tile - s_tp[g];
-    const int mi = local % mt, ni = local / mt;
-    const int row0 = row0g + mi * BM;
+    const int local = tile - __builtin_amdgcn_readfirstlane(s_tp[g]);
+    // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
+    // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
+    // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
+    const int band = local / (BAND_M * tiles_n);
+    const int bm0 = band * BAND_M;
+    const int bmt = min(BAND_M, mt - bm0);
+    const int in_band = local - band * BAND_M * tiles_n;
+    const int mi = bm0 + in_band % bmt;
+    ni = in_band / bmt;
+    row0 = row0g + mi * BM;
     const bf16_t* Wg = p.W + (int64_t)g * p.w_group_stride;
-
-    // ---- per-thread global chunk pointers ----
-    const bf16_t* xp[XCH];
-    int xs[XCH];
+    xbase = reinterpret_cast<const char*>(p.X + (int64_t)row0 * p.ldx);
+    const int last = row_end - 1 - row0;
 #pragma unroll
-    for (int i = 0; i < XCH; ++i) {
-      int c = tid + i * NT, r = c >> 3, ch = c & 7;
-      int row = min(row0 + r, row_end - 1);
-      xp[i] = p.X + (int64_t)row * p.ldx + ch * 8;
-      xs[i] = swz(r, ch);
+    for (int j = 0; j < LX; ++j) {
+      const int r = (wave + NW * j) * ROWS_PER_INST + li_row;      // tile row
+      xchunk[j] = li_pc ^ S::f(r);
+      xoff[j] = (uint32_t)(min(r, last) * p.ldx * 2 + xchunk[j] * 16);
     }
-    const bf16_t* wp[WCH];
-    int ws[WCH];
 #pragma unroll
-    for (int i = 0; i < WCH; ++i) {
-      int c = tid + i * NT, r = c >> 3, ch = c & 7;
-      int wrow;
+    for (int j = 0; j < LW; ++j) {
+      const int r = (wave + NW * j) * ROWS_PER_INST + li_row;
+      wchunk[j] = li_pc ^ S::f(r);
       if (EPI == EPI_SWIGLU) {
-        int half = r >= BN / 2;
-        int f = min(ni * (BN / 2) + (r - half * (BN / 2)), p.N - 1);
-        wrow = f + half * p.N;
+        const int half = ((wave + NW * j) * ROWS_PER_INST) >= BN / 2;   // uniform per instruction
+        const int f0 = ni * (BN / 2);
+        const int f = min(f0 + (r - half * (BN / 2)), p.N - 1);
+        wsb[j] = reinterpret_cast<const char*>(Wg + ((int64_t)f0 + half * p.N) * K);
+        woff[j] = (uint32_t)((f - f0) * K * 2 + wchunk[j] * 16);
       } else {
-        wrow = min(ni * BN + r, p.N - 1);
+        const int f0 = ni * BN;
+        const int f = min(f0 + r, p.N - 1);
+        wsb[j] = reinterpret_cast<const char*>(Wg + (int64_t)f0 * K);
+        woff[j] = (uint32_t)((f - f0) * K * 2 + wchunk[j] * 16);
       }
-      wp[i] = Wg + (int64_t)wrow * p.K + ch * 8;
-      ws[i] = swz(r, ch);
     }
+  };
 
-    const int nk = (p.K + BK - 1) / BK;
-    u32x4 rx[XCH], rw[WCH];
-    auto gload = [&](int kt) {
-      const int k0 = kt * BK;
+  // copy K slice kt of the current tile into ring slot st (L vector-memory ops per wave)
+  auto issue = [&](int kt, int st) {
+    bf16_t* dst = ring + st * SLICE;
+    const int k0b = kt * BK * 2;                           // byte offset of the slice
 #pragma unroll
-      for (int i = 0; i < XCH; ++i) {
-        int ch = (tid + i * NT) & 7;
-        rx[i] = (k0 + ch * 8 < p.K) ? ld16(xp[i] + k0) : u32x4{0, 0, 0, 0};
-      }
+    for (int j = 0; j < LX; ++j)
+      dma16(reinterpret_cast<const bf16_t*>(xbase + k0b + xoff[j]), dst + (wave + NW * j) * 512);
 #pragma unroll
-      for (int i = 0; i < WCH; ++i) {
-        int ch = (tid + i * NT) & 7;
-        rw[i] = (k0 + ch * 8 < p.K) ? ld16(wp[i] + k0) : u32x4{0, 0, 0, 0};
-      }
-    };
-    auto lstore = [&](int st) {
-      bf16_t* dX = sX + st * BM * BK;
-      bf16_t* dW = sW + st * BN * BK;
+    for (int j = 0; j < LW; ++j)
+      dma16(reinterpret_cast<const bf16_t*>(wsb[j] + k0b + woff[j]), dst + BM * BK + (wave + NW * j) * 512);
+  };
+  // the partial last slice (K % BK != 0): chunks past K are fetched from K-8 and zeroed later
+  auto issue_tail = [&](int kt, int st) {
+    bf16_t* dst = ring + st * SLICE;
+    const int k0 = kt * BK;
 #pragma unroll
-      for (int i = 0; i < XCH; ++i) st16(dX + xs[i], rx[i]);
+    for (int j = 0; j < LX; ++j) {
+      const int back = max(k0 + xchunk[j] * 8 - (K - 8), 0) * 2;
+      dma16(reinterpret_cast<const bf16_t*>(xbase + k0 * 2 + xoff[j] - back), dst + (wave + NW * j) * 512);
+    }
 #pragma unroll
-      for (int i = 0; i < WCH; ++i) st16(dW + ws[i], rw[i]);
-    };
+    for (int j = 0; j < LW; ++j) {
+      const int back = max(k0 + wchunk[j] * 8 - (K - 8), 0) * 2;
+      dma16(reinterpret_cast<const bf16_t*>(wsb[j] + k0 * 2 + woff[j] - back), dst + BM * BK + (wave + NW * j) * 512);
+    }
+  };
+  const int nk_full = K / BK;
+  auto issue_any = [&](int kt, int st) {
+    if constexpr (KTAIL) {
+      if (kt >= nk_full) { issue_tail(kt, st); return; }
+    }
+    issue(kt, st);
+  };
 
+  // make slice kt readable by every wave and refill the ring slot that slice kt-1 used
+  // (kt may be nk: then it only waits for every copy and synchronises)
+  auto sync_slice = [&](int kt) {
+    const int after = min(STAGES - 2, nk - 1 - kt);      // slices issued after kt
+    if (STAGES >= 4 && after >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * L : 0)>();
+    else if (STAGES >= 3 && after >= 1) wait_vmcnt<(STAGES >= 3 ? L : 0)>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (kt + STAGES - 1 < nk) issue_any(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    if (ktail && kt == nk - 1) {
+      // zero the chunks past K of the last slice (their copies came from clamped addresses)
+      bf16_t* z = ring + (kt % STAGES) * SLICE;
+      for (int idx = tid; idx < (BM + BN) * S::CPR; idx += NTH) {
+        const int r = idx / S::CPR, pc = idx % S::CPR;
+        const int c = pc ^ S::f(r);
+        if (kt * BK + c * 8 >= K) st16(z + r * BK + pc * 8, u32x4{0, 0, 0, 0});
+      }
+      lds_barrier();
+    }
+  };
+
+  // per-lane LDS element offsets of this wave's fragment rows (chunk 0 of the row)
+  constexpr int KS = BK / 16;                             // MFMA K-steps per slice
+  int wrow_l[FN], xrow_l[FM], wf_l[FN], xf_l[FM];
+#pragma unroll
+  for (int b = 0; b < FN; ++b) {
+    const int r = wbase[b] + (lane & 31);
+    wrow_l[b] = BM * BK + r * BK;
+    wf_l[b] = S::f(r);
+  }
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    const int r = wm * WM + a * 32 + (lane & 31);
+    xrow_l[a] = r * BK;
+    xf_l[a] = S::f(r);
+  }
+  const int hi = lane >> 5;
+  bf16x8 fw[2][FN], fx[2][FM];
+  auto load_frags = [&](int buf, int st, int ks) {
+    const bf16_t* base = ring + st * SLICE;
+    const int c = ks * 2 + hi;
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+      fw[buf][b] = *reinterpret_cast<const bf16x8*>(base + wrow_l[b] + ((c ^ wf_l[b]) << 3));
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+      fx[buf][a] = *reinterpret_cast<const bf16x8*>(base + xrow_l[a] + ((c ^ xf_l[a]) << 3));
+  };
+
+  int tile = slot;
+  if (tile >= total) return;
+  int row0, row_end, ni;
+  setup_tile(tile, row0, row_end, ni);
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue_any(s, s);
+
+  while (true) {
     f32x16 acc[FM][FN];
 #pragma unroll
     for (int a = 0; a < FM; ++a)
@@ -188,55 +351,59 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
 
-    // weight-row base of each fragment of this wave
-    int wbase[FN];
-#pragma unroll
-    for (int b = 0; b < FN; ++b) {
-      if (EPI == EPI_SWIGLU)
-        wbase[b] = (b < FN / 2) ? wn * (BN / 4) + b * 32 : BN / 2 + wn * (BN / 4) + (b - FN / 2) * 32;
-      else
-        wbase[b] = wn * WN + b * 32;
-    }
-
-    __syncthreads();            // previous tile's last LDS reads are done
-    gload(0);
-    lstore(0);
-    __syncthreads();
+    sync_slice(0);
+    load_frags(0, 0, 0);
     for (int kt = 0; kt < nk; ++kt) {
-      const int st = kt & 1;
-      if (kt + 1 < nk) gload(kt + 1);
-      const bf16_t* cX = sX + st * BM * BK;
-      const bf16_t* cW = sW + st * BN * BK;
+      const int st = kt % STAGES;
 #pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        const int ch = ks * 2 + (lane >> 5);
-        bf16x8 fw[FN], fx[FM];
-#pragma unroll
-        for (int b = 0; b < FN; ++b) fw[b] = lds_frag(cW, wbase[b] + (lane & 31), ch);
-#pragma unroll
-        for (int a = 0; a < FM; ++a) fx[a] = lds_frag(cX, wm * WM + a * 32 + (lane & 31), ch);
+      for (int ks = 0; ks < KS; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < KS) {
+          load_frags(cur ^ 1, st, ks + 1);
+        } else {
+          // the last step's fragments are in registers: publish the next slice now, so the
+          // barrier and the first reads of the next slice overlap this step's MFMAs (after
+          // the final slice this reads a stale ring slot, harmlessly, to keep the loop
+          // free of branches the wait-count insertion would have to merge)
+          sync_slice(kt + 1);
+          load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
+        }
 #pragma unroll
         for (int a = 0; a < FM; ++a)
 #pragma unroll
           for (int b = 0; b < FN; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[b], fx[a], acc[a][b], 0, 0, 0);
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+        // scheduling: an MFMA first (its operands were read during the previous step), then
+        // the next step's LDS reads two at a time between MFMAs, so every read has several
+        // MFMAs of this step to hide its latency behind
+        sched_step<FM + FN, FM * FN>();
       }
-      if (kt + 1 < nk) lstore(st ^ 1);
-      __syncthreads();
+    }
+
+    // next tile: start its copies before this tile's epilogue (every wave is done with the ring)
+    const int c_row0 = row0, c_row_end = row_end, c_ni = ni;
+    tile += G;
+    const bool more = tile < total;
+    lds_barrier();
+    if (more) {
+      setup_tile(tile, row0, row_end, ni);
+#pragma unroll
+      for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue_any(s, s);
     }
 
     // ---- epilogue: lane holds token column (lane & 31); features 8q + 4(lane>>5) + 0..3 ----
 #pragma unroll
     for (int a = 0; a < FM; ++a) {
-      const int row = row0 + wm * WM + a * 32 + (lane & 31);
-      if (row >= row_end) continue;
+      const int row = c_row0 + wm * WM + a * 32 + (lane & 31);
+      if (row >= c_row_end) continue;
       if (EPI == EPI_SWIGLU) {
         bf16_t* yrow = reinterpret_cast<bf16_t*>(p.Y) + (int64_t)row * p.ldy;
 #pragma unroll
         for (int b = 0; b < FN / 2; ++b) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int col = ni * (BN / 2) + wn * (BN / 4) + b * 32 + 8 * q + 4 * (lane >> 5);
+            const int col = c_ni * (BN / 2) + wn * HALF_W + b * 32 + 8 * q + 4 * (lane >> 5);
             if (col >= p.N) continue;
             float o[4];
 #pragma unroll
@@ -256,7 +423,7 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
         for (int b = 0; b < FN; ++b) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int col = ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
+            const int col = c_ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
             if (col >= p.N) continue;
             uint2 v;
             v.x = pack_bf16x2(acc[a][b][4 * q + 0], acc[a][b][4 * q + 1]);
@@ -270,7 +437,7 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
         for (int b = 0; b < FN; ++b) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int col = ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
+            const int col = c_ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if (col + e < p.N) yrow[col + e] = acc[a][b][4 * q + e];
@@ -278,6 +445,7 @@ __global__ __launch_bounds__(NT) void k_grouped_gemm(GemmProblem p) {
         }
       }
     }
+    if (!more) break;
   }
 }
 
@@ -305,39 +473,87 @@ DevInfo& dev_info() {
 int cu_count() { return dev_info().cus; }
 int lds_limit() { return dev_info().lds; }
 
-template <int BM, int BN, int EPI>
-hipError_t launch_tile(const GemmProblem& p, hipStream_t stream) {
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
+hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
+  constexpr int NTH = 64 * WGM * WGN;
   constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
-  const size_t lds = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
-  if (lds + 2 * (kMaxGroups + 1) * sizeof(int) + 64 > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
-  static bool attr_set = false;   // idempotent attribute, racing writers store the same value
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, EPI>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  const void* fn = reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>);
+  const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t);
+  const size_t lds_static = 2 * (kMaxGroups + 1) * sizeof(int) + 64;
+  if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
+  static int per_cu = 0;   // resident workgroups per CU (idempotent; racing writers store the same value)
+  if (per_cu == 0) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    int occ = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, NTH, lds);
+    if (e != hipSuccess) return e;
+    per_cu = occ > 0 ? occ : 1;
   }
   const int64_t tiles_n = (p.N + OUTN - 1) / OUTN;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
   const int64_t upper = tiles_n * ((rows + BM - 1) / BM + groups);
-  const int64_t resident = (int64_t)cu_count() * 2;
+  const int64_t resident = (int64_t)cu_count() * per_cu;
   int64_t grid = upper < resident ? upper : resident;
   if (grid >= 8) grid -= grid % 8;
   if (grid < 1) grid = 1;
-  hipLaunchKernelGGL((k_grouped_gemm<BM, BN, EPI>), dim3((unsigned)grid), dim3(NT), lds, stream, p);
+  hipLaunchKernelGGL((k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>), dim3((unsigned)grid), dim3(NTH),
+                     lds, stream, p);
   return hipGetLastError();
 }
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI>
+hipError_t launch_tile(const GemmProblem& p, hipStream_t stream) {
+  if (p.K < 8) return hipErrorInvalidValue;
+  if (p.K % BK == 0) return launch_kernel<BM, BN, BK, STAGES, WGM, WGN, EPI, false>(p, stream);
+  return launch_kernel<BM, BN, BK, STAGES, WGM, WGN, EPI, true>(p, stream);
+}
+
+template <int EPI>
+hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
+  switch (cfg) {
+    case 0: return launch_tile<128, 128, 64, 2, 2, 2, EPI>(p, stream);
+    case 1: return launch_tile<128, 256, 64, 3, 2, 2, EPI>(p, stream);
+    case 2: return launch_tile<256, 256, 64, 2, 2, 4, EPI>(p, stream);
+    case 3: return launch_tile<256, 256, 32, 4, 2, 4, EPI>(p, stream);
+    case 4: return launch_tile<128, 512, 32, 3, 2, 4, EPI>(p, stream);
+    case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI>(p, stream);
+    case 6: return launch_tile<256, 256, 64, 2, 4, 2, EPI>(p, stream);
+    case 7: return launch_tile<256, 128, 64, 3, 4, 2, EPI>(p, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+#ifdef MOE_GEMM_SWEEP
+int g_force_cfg[3] = {-1, -1, -1};
+#endif
 
 }  // namespace
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
+  // 256 x 256 tiles, 8 waves, two 64-wide K slices in flight: the best measured on the DeepSeek-V3,
+  // Mixtral and skewed workloads (largest reuse per byte copied into LDS)
+  int cfg_swiglu = 6, cfg_bf16 = 6;
+#ifdef MOE_GEMM_SWEEP
+  if (g_force_cfg[EPI_SWIGLU] >= 0) cfg_swiglu = g_force_cfg[EPI_SWIGLU];
+  if (g_force_cfg[EPI_BF16] >= 0) cfg_bf16 = g_force_cfg[EPI_BF16];
+#endif
   switch (p.epi) {
-    case EPI_SWIGLU: return launch_tile<128, 128, EPI_SWIGLU>(p, stream);
-    case EPI_BF16: return launch_tile<128, 128, EPI_BF16>(p, stream);
-    case EPI_F32: return launch_tile<64, 64, EPI_F32>(p, stream);
+    case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
+    case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
+    case EPI_F32: return launch_tile<64, 64, 64, 3, 2, 2, EPI_F32>(p, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace moe
+
+#ifdef MOE_GEMM_SWEEP
+// tile-configuration override for tuning sweeps (not part of the ABI)
+extern "C" int moe_sweep_set_gemm_cfg(int epi, int cfg) {
+  if (epi < 0 || epi > 2) return 1;
+  moe::g_force_cfg[epi] = cfg;
+  return 0;
+}
+#endif
