@@ -28,33 +28,54 @@ __global__ __launch_bounds__(256) void k_combine(CombineProblem p) {
       w[j] = p.topk_w[t * k + j];
     }
   }
+  constexpr int U = 4;                       // 16-byte vectors per lane in flight per row
   const int nvec = p.d / 8;
-  for (int v = lane; v < nvec; v += 64) {
-    float acc[8];
+  for (int v0 = 0; v0 < nvec; v0 += 64 * U) {
+    float acc[U][8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[u][e] = 0.f;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (rows[j] < 0) continue;
-      const u32x4 y = ld16(p.y_perm + (int64_t)rows[j] * p.d + v * 8);
+      const bf16_t* yrow = p.y_perm + (int64_t)rows[j] * p.d;
+      u32x4 y[U];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += w[j] * bf16_to_f32(y[e] & 0xffffu);
-        acc[2 * e + 1] += w[j] * bf16_to_f32(y[e] >> 16);
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + u * 64 + lane;
+        y[u] = v < nvec ? ld16(yrow + v * 8) : u32x4{0, 0, 0, 0};
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[u][2 * e] += w[j] * bf16_to_f32(y[u][e] & 0xffffu);
+          acc[u][2 * e + 1] += w[j] * bf16_to_f32(y[u][e] >> 16);
+        }
     }
     if (p.shared_y) {
-      const u32x4 s = ld16(p.shared_y + t * p.d + v * 8);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += bf16_to_f32(s[e] & 0xffffu);
-        acc[2 * e + 1] += bf16_to_f32(s[e] >> 16);
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + u * 64 + lane;
+        if (v >= nvec) continue;
+        const u32x4 sy = ld16(p.shared_y + t * p.d + v * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[u][2 * e] += bf16_to_f32(sy[e] & 0xffffu);
+          acc[u][2 * e + 1] += bf16_to_f32(sy[e] >> 16);
+        }
       }
     }
-    u32x4 o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
-    st16(p.out + t * p.d + v * 8, o);
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + u * 64 + lane;
+      if (v >= nvec) continue;
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(acc[u][2 * e], acc[u][2 * e + 1]);
+      st16(p.out + t * p.d + v * 8, o);
+    }
   }
 }
 

@@ -1,16 +1,16 @@
 // Histogram, prefix scan and stable permutation of the local (token, expert) slots.
 //
-// Tokens are cut into chunks of 64 (one wavefront).  Three launches:
+// Tokens are cut into chunks of 64 (one wavefront).  Four launches:
 //   k_chunk_count  per chunk, how many of its slots go to each local expert
 //   k_chunk_scan   per expert, exclusive scan of the chunk counts over chunks, and
 //                  the expert total (counts[e])
-//   k_permute      per chunk: the offsets (exclusive scan of counts, the monotone
+//   k_rank         per chunk: the offsets (exclusive scan of counts, the monotone
 //                  [E_local+1] array), each slot's rank among the chunk's earlier slots
 //                  of the same expert, hence its row
 //                      row = offsets[e] + chunk_base[c][e] + rank,
-//                  then row_token / slot_row, and the bit-exact copy of every token row
-//                  to each of its local rows (the token is read once, written k_local
-//                  times, 16-byte vectors).
+//                  then row_token / slot_row
+//   k_gather       per token: the bit-exact copy of the token row to each of its local
+//                  rows (read once, written k_local times, 16-byte vectors)
 //
 // The in-chunk rank uses wavefront ballots instead of atomics, so the order inside an
 // expert is ascending token (a stable counting sort) and run-to-run identical: for every
@@ -24,7 +24,6 @@ namespace moe {
 namespace {
 
 constexpr int CH = 64;          // tokens per chunk = lanes of one wave
-constexpr int kSub = 4;         // copy workgroups per chunk
 
 __global__ __launch_bounds__(64) void k_chunk_count(PermuteProblem p) {
   extern __shared__ int s_cnt[];   // [E_local]
@@ -72,17 +71,16 @@ __global__ __launch_bounds__(256) void k_chunk_scan(PermuteProblem p, int nblk) 
   if (tid == 0) p.counts[e] = carry;
 }
 
-// grid (nblk, kSub): workgroup (c, s) ranks chunk c and copies its s-th quarter of tokens
-__global__ __launch_bounds__(256) void k_permute(PermuteProblem p) {
-  extern __shared__ int s_dyn[];
-  int* s_off = s_dyn;                          // [E_local + 1]
-  int* s_row = s_dyn + p.E_local + 1;          // [CH * top_k]
+// one workgroup per chunk: offsets (every workgroup; workgroup 0 publishes them), then wave 0
+// ranks the chunk's slots and writes row_token / slot_row
+__global__ __launch_bounds__(256) void k_rank(PermuteProblem p) {
+  extern __shared__ int s_off[];               // [E_local + 1]
   __shared__ int s_w[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = blockIdx.x, sub = blockIdx.y;
+  const int c = blockIdx.x;
   const int E_local = p.E_local, k = p.top_k;
 
-  // offsets = exclusive scan of counts (every workgroup; workgroup (0,0) publishes it)
+  // offsets = exclusive scan of counts
   {
     constexpr int PER = 4;                     // 256 threads x 4 >= 1024 experts
     int v[PER], lsum = 0;
@@ -115,86 +113,96 @@ __global__ __launch_bounds__(256) void k_permute(PermuteProblem p) {
     }
     if (tid == 0) s_off[E_local] = tot;
     __syncthreads();
-    if (c == 0 && sub == 0)
+    if (c == 0)
       for (int e = tid; e <= E_local; e += 256) p.offsets[e] = s_off[e];
   }
+  if (wave != 0) return;
 
-  // rank of each slot inside the chunk (wave 0), rows to LDS
-  const int64_t t0 = (int64_t)c * CH;
-  if (wave == 0) {
-    const int64_t t = t0 + lane;
-    const bool valid_t = t < p.T;
-    int nbits = 0;
-    while ((1 << nbits) < E_local) ++nbits;
-    const int32_t* base = p.blk_base + (int64_t)c * E_local;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    int myle[16];
-    int rank[16];
+  // rank of each slot among the chunk's earlier slots of the same expert
+  const int64_t t = (int64_t)c * CH + lane;
+  const bool valid_t = t < p.T;
+  int nbits = 0;
+  while ((1 << nbits) < E_local) ++nbits;
+  const int32_t* base = p.blk_base + (int64_t)c * E_local;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int myle[16];
+  int rank[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      myle[j] = -1;
-      rank[j] = 0;
-      if (j < k && valid_t) {
-        const int le = p.topk_idx[t * k + j] - p.e_begin;
-        myle[j] = (le >= 0 && le < E_local) ? le : -1;
-      }
+  for (int j = 0; j < 16; ++j) {
+    myle[j] = -1;
+    rank[j] = 0;
+    if (j < k && valid_t) {
+      const int le = p.topk_idx[t * k + j] - p.e_begin;
+      myle[j] = (le >= 0 && le < E_local) ? le : -1;
     }
+  }
 #pragma unroll
-    for (int jp = 0; jp < 16; ++jp) {
-      if (jp >= k) break;
-      // lanes whose slot jp is local, and per bit the lanes whose slot jp has that bit set
-      const int lej = myle[jp];
-      const uint64_t vmask = __ballot(lej >= 0);
-      uint64_t bal[10];
+  for (int jp = 0; jp < 16; ++jp) {
+    if (jp >= k) break;
+    // lanes whose slot jp is local, and per bit the lanes whose slot jp has that bit set
+    const int lej = myle[jp];
+    const uint64_t vmask = __ballot(lej >= 0);
+    uint64_t bal[10];
 #pragma unroll
-      for (int b = 0; b < 10; ++b) bal[b] = (b < nbits) ? __ballot(lej >= 0 && ((lej >> b) & 1)) : 0ull;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (j >= k) break;
-        const int le = myle[j];
-        uint64_t m = vmask;
-#pragma unroll
-        for (int b = 0; b < 10; ++b)
-          if (b < nbits) m &= ((le >> b) & 1) ? bal[b] : ~bal[b];
-        rank[j] += __popcll(m & below);
-      }
-    }
+    for (int b = 0; b < 10; ++b) bal[b] = (b < nbits) ? __ballot(lej >= 0 && ((lej >> b) & 1)) : 0ull;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (j >= k) break;
-      int row = -1;
-      if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[j];
-      if (row >= p.cap) row = -1;            // unreachable for a consistent histogram; keeps writes in bounds
-      s_row[lane * k + j] = row;
-      if (sub == 0 && valid_t) {
-        p.slot_row[t * k + j] = row;
-        if (row >= 0) p.row_token[row] = (int32_t)t;
-      }
+      const int le = myle[j];
+      uint64_t m = vmask;
+#pragma unroll
+      for (int b = 0; b < 10; ++b)
+        if (b < nbits) m &= ((le >> b) & 1) ? bal[b] : ~bal[b];
+      rank[j] += __popcll(m & below);
     }
   }
-  __syncthreads();
+  if (!valid_t) return;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    if (j >= k) break;
+    int row = -1;
+    if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[j];
+    if (row >= p.cap) row = -1;              // unreachable for a consistent histogram; keeps writes in bounds
+    p.slot_row[t * k + j] = row;
+    if (row >= 0) p.row_token[row] = (int32_t)t;
+  }
+}
 
-  // copy: each wave takes tokens of this workgroup's quarter; 16-byte vectors
-  const int per_sub = CH / kSub;
+// one wave per token: the token row is read once (16-byte vectors, U per lane in flight)
+// and written to each of its local rows
+__global__ __launch_bounds__(256) void k_gather(PermuteProblem p) {
+  constexpr int U = 8;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= p.T) return;
+  const int k = p.top_k;
+  int rows[16];
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    rows[j] = (j < k) ? p.slot_row[t * k + j] : -1;
+    if (rows[j] >= p.cap) rows[j] = -1;
+    any |= rows[j] >= 0;
+  }
+  if (!any) return;
   const int nvec = p.d / 8;
-  for (int i = wave; i < per_sub; i += 4) {
-    const int l = sub * per_sub + i;
-    const int64_t t = t0 + l;
-    if (t >= p.T) break;
-    int rows[16];
-    bool any = false;
+  const u32x4* src = reinterpret_cast<const u32x4*>(p.x + t * p.d);
+  for (int v0 = 0; v0 < nvec; v0 += 64 * U) {
+    u32x4 val[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + u * 64 + lane;
+      if (v < nvec) val[u] = src[v];
+    }
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      rows[j] = (j < k) ? s_row[l * k + j] : -1;
-      any |= rows[j] >= 0;
-    }
-    if (!any) continue;
-    const u32x4* src = reinterpret_cast<const u32x4*>(p.x + t * p.d);
-    for (int v = lane; v < nvec; v += 64) {
-      const u32x4 val = src[v];
+      if (rows[j] < 0) continue;
+      u32x4* dst = reinterpret_cast<u32x4*>(p.x_perm + (int64_t)rows[j] * p.d);
 #pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (rows[j] >= 0) reinterpret_cast<u32x4*>(p.x_perm + (int64_t)rows[j] * p.d)[v] = val;
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + u * 64 + lane;
+        if (v < nvec) dst[v] = val[u];
+      }
     }
   }
 }
@@ -212,8 +220,10 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*bet
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (between && between() != 0) return hipErrorUnknown;
-  const size_t lds = (size_t)(p.E_local + 1 + CH * p.top_k) * sizeof(int);
-  hipLaunchKernelGGL(k_permute, dim3((unsigned)nblk, kSub), dim3(256), lds, stream, p);
+  hipLaunchKernelGGL(k_rank, dim3((unsigned)nblk), dim3(256), (p.E_local + 1) * sizeof(int), stream, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gather, dim3((unsigned)((p.T + 3) / 4)), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
