@@ -199,6 +199,8 @@ typedef enum moe_step {
   MOE_STEP_FFN_DOWN = 5,      /* routed experts: W2 GEMM                            */
   MOE_STEP_SHARED_UP = 6,     /* shared expert: W1/W3 GEMM + SwiGLU (if F_shared)   */
   MOE_STEP_SHARED_DOWN = 7,   /* shared expert: W2 GEMM (if F_shared)               */
+  /* when F_shared == F the shared expert runs inside the two routed launches (steps 4 and 5
+     then cover both and steps 6 and 7 are empty) */
   MOE_STEP_COMBINE = 8,       /* gate-weighted combine                              */
   MOE_STEP_COUNT_ = 9
 } moe_step_t;

@@ -223,8 +223,19 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
                     "permute launch");
 }
 
+// Shared expert run inside the routed launches (an extra GEMM group on its own operands).
+struct SharedOperands {
+  const void* x = nullptr;    // [T, d]
+  const void* w13 = nullptr;  // [2F, d]
+  const void* w2 = nullptr;   // [d, F]
+  void* act = nullptr;        // [T, F]
+  void* y = nullptr;          // [T, d]
+  int64_t T = 0;
+};
+
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
-           int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0) {
+           int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0,
+           const SharedOperands* sh = nullptr) {
   moe::GemmProblem up{};
   up.X = static_cast<const moe::bf16_t*>(X);
   up.ldx = d;
@@ -239,6 +250,12 @@ int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, cons
   up.Y = act;
   up.ldy = F;
   up.epi = moe::EPI_SWIGLU;
+  if (sh) {
+    up.X2 = static_cast<const moe::bf16_t*>(sh->x);
+    up.W2 = static_cast<const moe::bf16_t*>(sh->w13);
+    up.Y2 = sh->act;
+    up.rows2 = (int32_t)sh->T;
+  }
   CHECK(hip_status(moe::launch_grouped_gemm(up, st), "expert up-projection launch"));
   if (mark) CHECK(mark(down_step));
   moe::GemmProblem dn = up;
@@ -251,6 +268,12 @@ int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, cons
   dn.Y = y;
   dn.ldy = d;
   dn.epi = moe::EPI_BF16;
+  if (sh) {
+    dn.X2 = static_cast<const moe::bf16_t*>(sh->act);
+    dn.W2 = static_cast<const moe::bf16_t*>(sh->w2);
+    dn.Y2 = sh->y;
+    dn.rows2 = (int32_t)sh->T;
+  }
   return hip_status(moe::launch_grouped_gemm(dn, st), "expert down-projection launch");
 }
 
@@ -414,11 +437,23 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
   if (mark) CHECK(mark(MOE_STEP_HISTOGRAM));
   CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, at<void>(ws, L.perm_ws), st,
                    mark));
+  // a shared expert as wide as the routed ones runs inside the routed launches (its tiles
+  // interleaved with the experts'), otherwise in launches of its own
+  const bool merged = shape->F_shared > 0 && shape->F_shared == shape->F;
+  SharedOperands so;
+  if (merged) {
+    so.x = x;
+    so.w13 = ws13;
+    so.w2 = ws2;
+    so.act = at<void>(ws, L.act_s);
+    so.y = shared_y;
+    so.T = shape->T;
+  }
   if (mark) CHECK(mark(MOE_STEP_FFN_UP));
   CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, at<void>(ws, L.act),
-               y_perm, st, mark, MOE_STEP_FFN_DOWN));
+               y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr));
   if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
-  if (shape->F_shared > 0)
+  if (shape->F_shared > 0 && !merged)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,
                  st, mark, MOE_STEP_SHARED_DOWN));
   else if (mark)

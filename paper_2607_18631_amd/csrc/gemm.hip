@@ -163,15 +163,20 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     lsum += loc[i];
   }
   int excl;
-  const int total = block_exclusive_scan<NTH>(lsum, s_tmp, excl);
+  const int total_r = block_exclusive_scan<NTH>(lsum, s_tmp, excl);
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     int g = tid * PER + i;
     if (g < groups) s_tp[g] = excl;
     excl += loc[i];
   }
-  if (tid == 0) s_tp[groups] = total;
+  if (tid == 0) s_tp[groups] = total_r;
   __syncthreads();
+  // the extra group's tiles are spread evenly among the grouped ones (position t is an extra
+  // tile iff floor((t+1) S / total) > floor(t S / total)), so HBM-bound expert tiles and
+  // compute-bound shared-expert tiles run side by side
+  const int tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * tiles_n : 0;
+  const int total = total_r + tiles_x;
 
   const int G = gridDim.x;
   const int slot = (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
@@ -198,21 +203,40 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   // cost one scalar add each and no vector ALU.  The W instruction j is uniformly in the gate
   // or the up half of a SwiGLU tile.
   const char* xbase;
+  void* ytile;
   const char* wsb[LW];
   uint32_t xoff[LX], woff[LW];
   int xchunk[LX], wchunk[LW];
 
   auto setup_tile = [&](int tile, int& row0, int& row_end, int& ni) {
-    int lo = 0, hi = groups;                              // s_tp[groups] == total > tile
-    while (hi - lo > 1) {
-      int mid = (lo + hi) >> 1;
-      if (s_tp[mid] <= tile) lo = mid; else hi = mid;
+    const int x_before = (int)((int64_t)tile * tiles_x / total);
+    const bool extra = (int)((int64_t)(tile + 1) * tiles_x / total) > x_before;
+    int row0g, local;
+    const bf16_t* Wg;
+    const bf16_t* Xg;
+    if (extra) {
+      row0g = 0;
+      row_end = p.rows2;
+      local = x_before;
+      Wg = p.W2;
+      Xg = p.X2;
+      ytile = p.Y2;
+    } else {
+      const int t = tile - x_before;                      // index among the grouped tiles
+      int lo = 0, hi = groups;                            // s_tp[groups] == total_r > t
+      while (hi - lo > 1) {
+        int mid = (lo + hi) >> 1;
+        if (s_tp[mid] <= t) lo = mid; else hi = mid;
+      }
+      const int g = __builtin_amdgcn_readfirstlane(lo);
+      row0g = __builtin_amdgcn_readfirstlane(s_off[g]);
+      row_end = __builtin_amdgcn_readfirstlane(s_off[g + 1]);
+      local = t - __builtin_amdgcn_readfirstlane(s_tp[g]);
+      Wg = p.W + (int64_t)g * p.w_group_stride;
+      Xg = p.X;
+      ytile = p.Y;
     }
-    const int g = __builtin_amdgcn_readfirstlane(lo);
-    const int row0g = __builtin_amdgcn_readfirstlane(s_off[g]);
-    row_end = __builtin_amdgcn_readfirstlane(s_off[g + 1]);
     const int mt = (row_end - row0g + BM - 1) / BM;
-    const int local = tile - __builtin_amdgcn_readfirstlane(s_tp[g]);
     // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
     // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
     // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
@@ -223,8 +247,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     const int mi = bm0 + in_band % bmt;
     ni = in_band / bmt;
     row0 = row0g + mi * BM;
-    const bf16_t* Wg = p.W + (int64_t)g * p.w_group_stride;
-    xbase = reinterpret_cast<const char*>(p.X + (int64_t)row0 * p.ldx);
+    xbase = reinterpret_cast<const char*>(Xg + (int64_t)row0 * p.ldx);
     const int last = row_end - 1 - row0;
 #pragma unroll
     for (int j = 0; j < LX; ++j) {
@@ -280,9 +303,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   const int nk_full = K / BK;
   auto issue_any = [&](int kt, int st) {
     if constexpr (KTAIL) {
-      if (kt >= nk_full) { issue_tail(kt, st); return; }
+      if (kt >= nk_full) issue_tail(kt, st);
+      else issue(kt, st);
+    } else {
+      issue(kt, st);
     }
-    issue(kt, st);
   };
 
   // make slice kt readable by every wave and refill the ring slot that slice kt-1 used
@@ -382,6 +407,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
 
     // next tile: start its copies before this tile's epilogue (every wave is done with the ring)
     const int c_row0 = row0, c_row_end = row_end, c_ni = ni;
+    void* const c_y = ytile;
     tile += G;
     const bool more = tile < total;
     lds_barrier();
@@ -398,7 +424,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       const int row = c_row0 + wm * WM + a * 32 + (lane & 31);
       if (row >= c_row_end) continue;
       if (EPI == EPI_SWIGLU) {
-        bf16_t* yrow = reinterpret_cast<bf16_t*>(p.Y) + (int64_t)row * p.ldy;
+        bf16_t* yrow = reinterpret_cast<bf16_t*>(c_y) + (int64_t)row * p.ldy;
 #pragma unroll
         for (int b = 0; b < FN / 2; ++b) {
 #pragma unroll
@@ -418,7 +444,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
           }
         }
       } else if (EPI == EPI_BF16) {
-        bf16_t* yrow = reinterpret_cast<bf16_t*>(p.Y) + (int64_t)row * p.ldy;
+        bf16_t* yrow = reinterpret_cast<bf16_t*>(c_y) + (int64_t)row * p.ldy;
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
 #pragma unroll
@@ -432,7 +458,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
           }
         }
       } else {
-        float* yrow = reinterpret_cast<float*>(p.Y) + (int64_t)row * p.ldy;
+        float* yrow = reinterpret_cast<float*>(c_y) + (int64_t)row * p.ldy;
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
 #pragma unroll
@@ -493,7 +519,7 @@ hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
   const int64_t tiles_n = (p.N + OUTN - 1) / OUTN;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
-  const int64_t upper = tiles_n * ((rows + BM - 1) / BM + groups);
+  const int64_t upper = tiles_n * ((rows + BM - 1) / BM + groups + (p.rows2 + BM - 1) / BM);
   const int64_t resident = (int64_t)cu_count() * per_cu;
   int64_t grid = upper < resident ? upper : resident;
   if (grid >= 8) grid -= grid % 8;

@@ -29,6 +29,12 @@ struct GemmProblem {
   void* Y;                    // bf16 or f32 output, row stride ldy (elements)
   int64_t ldy;
   int32_t epi;
+  // optional extra group on its own operands (the shared expert run inside the routed launch):
+  // rows [0, rows2) of X2 against W2 into Y2, same N, K, ldx and ldy; rows2 = 0 means none
+  const bf16_t* X2;
+  const bf16_t* W2;
+  void* Y2;
+  int32_t rows2;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
