@@ -32,7 +32,13 @@
 //
 // Edges: token rows past the group's end and weight rows past N are clamped to the last
 // valid row (their results are never stored); a K tail (K % BK != 0) is fetched from
-// clamped addresses and its chunks past K are zeroed in LDS before use.
+// clamped addresses and its chunks past K are zeroed in LDS before use.  The 32-row token
+// blocks of a tile alternate over the waves, and a wave runs no MFMA for its blocks past
+// the group's end, so the ragged last m-tile of an expert costs MFMA time in proportion to
+// its live rows (the per-expert row counts of a routed batch scatter around the mean,
+// which leaves most experts with one mostly empty m-tile).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -111,37 +117,24 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
   return total;
 }
 
-// BM token rows x BN weight rows per tile, WGM x WGN waves (each a (BM/WGM) x (BN/WGN)
-// sub-tile), BK-wide K slices through a STAGES-deep ring.
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem p) {
-  using S = Swz<BK>;
-  constexpr int NW = WGM * WGN, NTH = 64 * NW;
-  constexpr int WM = BM / WGM, WN = BN / WGN;             // per-wave sub-tile
-  constexpr int FM = WM / 32, FN = WN / 32;               // 32x32 fragments per wave
-  constexpr int ROWS_PER_INST = 1024 / (BK * 2);          // rows one wave instruction fills
-  constexpr int QX = BM / ROWS_PER_INST, QW = BN / ROWS_PER_INST;   // instructions per slice
-  constexpr int LX = QX / NW, LW = QW / NW;               // ... per wave
-  constexpr int L = LX + LW;                              // vector-memory ops per wave per slice
-  constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
-  constexpr int HALF_W = (EPI == EPI_SWIGLU) ? BN / 2 / WGN : WN;   // gate rows per wave (SwiGLU)
-  constexpr int SLICE = (BM + BN) * BK;                   // bf16 elements per ring slot
-  static_assert(FM >= 1 && FN >= 1 && QX % NW == 0 && QW % NW == 0, "tile too small");
-  static_assert(EPI != EPI_SWIGLU || (FN % 2 == 0 && HALF_W % 32 == 0), "SwiGLU pairs gate and up fragments");
-  static_assert(STAGES >= 2 && (STAGES - 2) * L < 64, "ring depth");
+// ---------------------------------------------------------------------------------------
+// Tile table, tile decoding, slice copies, epilogue
+// ---------------------------------------------------------------------------------------
 
-  extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* ring = reinterpret_cast<bf16_t*>(smem);         // [STAGES][BM + BN][BK]: X rows then W rows
-  __shared__ int s_off[kMaxGroups + 1];
-  __shared__ int s_tp[kMaxGroups + 1];
-  __shared__ int s_tmp[NTH / 64];
+// Tiles of one launch: `groups` row segments of BM-row tiles x tiles_n output tiles each,
+// plus tiles_x tiles of the optional extra group, `total` in all.  s_off / s_tp live in LDS.
+struct TileSpace {
+  int groups, tiles_n, tiles_x, total;
+  const int* s_off;          // [groups + 1] row offsets clamped to [0, max_rows]
+  const int* s_tp;           // [groups + 1] first tile of each group; s_tp[groups] = grouped tiles
+};
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int tiles_n = (p.N + OUTN - 1) / OUTN;
-
-  // ---- tile table: s_tp[g] = first tile of group g ----
+// Build the launch's tile table in LDS (every thread of the block calls this).
+template <int NTH, int BM>
+__device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off, int* s_tp, int* s_tmp) {
+  const int tid = threadIdx.x;
+  TileSpace ts;
+  ts.tiles_n = (p.N + outn - 1) / outn;
   int groups = p.groups;
   if (p.offsets) {
     // clamp to [0, max_rows]: any offsets content keeps every access inside the buffers
@@ -159,7 +152,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   for (int i = 0; i < PER; ++i) {
     int g = tid * PER + i;
     int m = g < groups ? max(s_off[g + 1] - s_off[g], 0) : 0;
-    loc[i] = ((m + BM - 1) / BM) * tiles_n;
+    loc[i] = ((m + BM - 1) / BM) * ts.tiles_n;
     lsum += loc[i];
   }
   int excl;
@@ -175,108 +168,122 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   // the extra group's tiles are spread evenly among the grouped ones (position t is an extra
   // tile iff floor((t+1) S / total) > floor(t S / total)), so HBM-bound expert tiles and
   // compute-bound shared-expert tiles run side by side
-  const int tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * tiles_n : 0;
-  const int total = total_r + tiles_x;
+  ts.tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * ts.tiles_n : 0;
+  ts.total = total_r + ts.tiles_x;
+  ts.groups = groups;
+  ts.s_off = s_off;
+  ts.s_tp = s_tp;
+  return ts;
+}
 
+// Workgroup b's first tile: adjacent tiles go to workgroups of one XCD (b runs on XCD b % 8).
+__device__ __forceinline__ int first_tile_slot() {
   const int G = gridDim.x;
-  const int slot = (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
-  const int K = p.K;
-  const int nk = (K + BK - 1) / BK;
-  constexpr bool ktail = KTAIL;                           // K % BK != 0 (launcher-checked)
+  return (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+}
 
-  // lane's position inside one wave instruction: row offset and physical chunk
-  const int li_row = lane / S::CPR;                       // 0 .. ROWS_PER_INST-1
-  const int li_pc = lane % S::CPR;
+// One tile: token rows [row0, min(row0 + BM, row_end)) of operand X against output tile ni
+// of the weights W, results into Y.
+struct TileDesc {
+  int row0, row_end, ni;
+  const bf16_t* X;
+  const bf16_t* W;
+  void* Y;
+};
 
-  // weight-row base (inside the W tile) of each fragment of this wave
-  int wbase[FN];
-#pragma unroll
-  for (int b = 0; b < FN; ++b) {
-    if (EPI == EPI_SWIGLU)
-      wbase[b] = (b < FN / 2) ? wn * HALF_W + b * 32 : BN / 2 + wn * HALF_W + (b - FN / 2) * 32;
-    else
-      wbase[b] = wn * WN + b * 32;
+template <int BM>
+__device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const TileSpace& ts, int tile) {
+  TileDesc d;
+  const int x_before = (int)((int64_t)tile * ts.tiles_x / ts.total);
+  const bool extra = (int)((int64_t)(tile + 1) * ts.tiles_x / ts.total) > x_before;
+  int row0g, local;
+  if (extra) {
+    row0g = 0;
+    d.row_end = p.rows2;
+    local = x_before;
+    d.W = p.W2;
+    d.X = p.X2;
+    d.Y = p.Y2;
+  } else {
+    const int t = tile - x_before;                        // index among the grouped tiles
+    int lo = 0, hi = ts.groups;                           // s_tp[groups] == grouped tiles > t
+    while (hi - lo > 1) {
+      int mid = (lo + hi) >> 1;
+      if (ts.s_tp[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int g = __builtin_amdgcn_readfirstlane(lo);
+    row0g = __builtin_amdgcn_readfirstlane(ts.s_off[g]);
+    d.row_end = __builtin_amdgcn_readfirstlane(ts.s_off[g + 1]);
+    local = t - __builtin_amdgcn_readfirstlane(ts.s_tp[g]);
+    d.W = p.W + (int64_t)g * p.w_group_stride;
+    d.X = p.X;
+    d.Y = p.Y;
   }
+  const int mt = (d.row_end - row0g + BM - 1) / BM;
+  // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
+  // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
+  // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
+  const int band = local / (BAND_M * ts.tiles_n);
+  const int bm0 = band * BAND_M;
+  const int bmt = min(BAND_M, mt - bm0);
+  const int in_band = local - band * BAND_M * ts.tiles_n;
+  const int mi = bm0 + in_band % bmt;
+  d.ni = in_band / bmt;
+  d.row0 = row0g + mi * BM;
+  return d;
+}
 
-  // Per-tile copy sources: a wave-uniform base (scalar registers) per copy instruction and a
-  // fixed per-lane 32-bit byte offset (row * ld + logical chunk), so a full slice's copies
-  // cost one scalar add each and no vector ALU.  The W instruction j is uniformly in the gate
-  // or the up half of a SwiGLU tile.
+// Copies of one K slice of a tile into a ring slot, spread over NW waves.  Per tile, a
+// wave-uniform base (scalar registers) per copy instruction and a fixed per-lane 32-bit byte
+// offset (row * ld + logical chunk), so a full slice's copies cost one scalar add each and
+// no vector ALU.  The W instruction j is uniformly in the gate or the up half of a SwiGLU
+// tile.  Token rows past the tile's end and weight rows past N are clamped to the last valid
+// row.
+template <int BM, int BN, int BK, int NW, int EPI>
+struct CopyPlan {
+  using Z = Swz<BK>;
+  static constexpr int RPI = 1024 / (BK * 2);              // rows one wave instruction fills
+  static constexpr int LX = BM / RPI / NW, LW = BN / RPI / NW;
+  static constexpr int L = LX + LW;                        // vector-memory ops per wave per slice
+  static_assert(LX >= 1 && LW >= 1 && (BM / RPI) % NW == 0 && (BN / RPI) % NW == 0, "tile too small");
+
   const char* xbase;
-  void* ytile;
   const char* wsb[LW];
   uint32_t xoff[LX], woff[LW];
   int xchunk[LX], wchunk[LW];
 
-  auto setup_tile = [&](int tile, int& row0, int& row_end, int& ni) {
-    const int x_before = (int)((int64_t)tile * tiles_x / total);
-    const bool extra = (int)((int64_t)(tile + 1) * tiles_x / total) > x_before;
-    int row0g, local;
-    const bf16_t* Wg;
-    const bf16_t* Xg;
-    if (extra) {
-      row0g = 0;
-      row_end = p.rows2;
-      local = x_before;
-      Wg = p.W2;
-      Xg = p.X2;
-      ytile = p.Y2;
-    } else {
-      const int t = tile - x_before;                      // index among the grouped tiles
-      int lo = 0, hi = groups;                            // s_tp[groups] == total_r > t
-      while (hi - lo > 1) {
-        int mid = (lo + hi) >> 1;
-        if (s_tp[mid] <= t) lo = mid; else hi = mid;
-      }
-      const int g = __builtin_amdgcn_readfirstlane(lo);
-      row0g = __builtin_amdgcn_readfirstlane(s_off[g]);
-      row_end = __builtin_amdgcn_readfirstlane(s_off[g + 1]);
-      local = t - __builtin_amdgcn_readfirstlane(s_tp[g]);
-      Wg = p.W + (int64_t)g * p.w_group_stride;
-      Xg = p.X;
-      ytile = p.Y;
-    }
-    const int mt = (row_end - row0g + BM - 1) / BM;
-    // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
-    // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
-    // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
-    const int band = local / (BAND_M * tiles_n);
-    const int bm0 = band * BAND_M;
-    const int bmt = min(BAND_M, mt - bm0);
-    const int in_band = local - band * BAND_M * tiles_n;
-    const int mi = bm0 + in_band % bmt;
-    ni = in_band / bmt;
-    row0 = row0g + mi * BM;
-    xbase = reinterpret_cast<const char*>(Xg + (int64_t)row0 * p.ldx);
-    const int last = row_end - 1 - row0;
+  __device__ __forceinline__ void setup(const GemmProblem& p, const TileDesc& t, int wave, int lane) {
+    const int li_row = lane / Z::CPR, li_pc = lane % Z::CPR;
+    const int K = p.K;
+    xbase = reinterpret_cast<const char*>(t.X + (int64_t)t.row0 * p.ldx);
+    const int last = t.row_end - 1 - t.row0;
 #pragma unroll
     for (int j = 0; j < LX; ++j) {
-      const int r = (wave + NW * j) * ROWS_PER_INST + li_row;      // tile row
-      xchunk[j] = li_pc ^ S::f(r);
+      const int r = (wave + NW * j) * RPI + li_row;         // tile row
+      xchunk[j] = li_pc ^ Z::f(r);
       xoff[j] = (uint32_t)(min(r, last) * p.ldx * 2 + xchunk[j] * 16);
     }
 #pragma unroll
     for (int j = 0; j < LW; ++j) {
-      const int r = (wave + NW * j) * ROWS_PER_INST + li_row;
-      wchunk[j] = li_pc ^ S::f(r);
+      const int r = (wave + NW * j) * RPI + li_row;
+      wchunk[j] = li_pc ^ Z::f(r);
       if (EPI == EPI_SWIGLU) {
-        const int half = ((wave + NW * j) * ROWS_PER_INST) >= BN / 2;   // uniform per instruction
-        const int f0 = ni * (BN / 2);
+        const int half = ((wave + NW * j) * RPI) >= BN / 2;  // uniform per instruction
+        const int f0 = t.ni * (BN / 2);
         const int f = min(f0 + (r - half * (BN / 2)), p.N - 1);
-        wsb[j] = reinterpret_cast<const char*>(Wg + ((int64_t)f0 + half * p.N) * K);
+        wsb[j] = reinterpret_cast<const char*>(t.W + ((int64_t)f0 + half * p.N) * K);
         woff[j] = (uint32_t)((f - f0) * K * 2 + wchunk[j] * 16);
       } else {
-        const int f0 = ni * BN;
+        const int f0 = t.ni * BN;
         const int f = min(f0 + r, p.N - 1);
-        wsb[j] = reinterpret_cast<const char*>(Wg + (int64_t)f0 * K);
+        wsb[j] = reinterpret_cast<const char*>(t.W + (int64_t)f0 * K);
         woff[j] = (uint32_t)((f - f0) * K * 2 + wchunk[j] * 16);
       }
     }
-  };
+  }
 
-  // copy K slice kt of the current tile into ring slot st (L vector-memory ops per wave)
-  auto issue = [&](int kt, int st) {
-    bf16_t* dst = ring + st * SLICE;
+  // copy K slice kt into the ring slot at dst (L vector-memory ops of this wave)
+  __device__ __forceinline__ void issue(bf16_t* dst, int kt, int wave) const {
     const int k0b = kt * BK * 2;                           // byte offset of the slice
 #pragma unroll
     for (int j = 0; j < LX; ++j)
@@ -284,10 +291,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
 #pragma unroll
     for (int j = 0; j < LW; ++j)
       dma16(reinterpret_cast<const bf16_t*>(wsb[j] + k0b + woff[j]), dst + BM * BK + (wave + NW * j) * 512);
-  };
+  }
+
   // the partial last slice (K % BK != 0): chunks past K are fetched from K-8 and zeroed later
-  auto issue_tail = [&](int kt, int st) {
-    bf16_t* dst = ring + st * SLICE;
+  __device__ __forceinline__ void issue_tail(bf16_t* dst, int kt, int wave, int K) const {
     const int k0 = kt * BK;
 #pragma unroll
     for (int j = 0; j < LX; ++j) {
@@ -299,14 +306,144 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       const int back = max(k0 + wchunk[j] * 8 - (K - 8), 0) * 2;
       dma16(reinterpret_cast<const bf16_t*>(wsb[j] + k0 * 2 + woff[j] - back), dst + BM * BK + (wave + NW * j) * 512);
     }
-  };
+  }
+};
+
+// First W-tile row of fragment b of a wave whose sub-tile is column block wn of WGN (each
+// wave owns the gate rows and the matching up rows of its features in a SwiGLU tile).
+template <int EPI, int BN, int WGN, int FN>
+__device__ __forceinline__ int frag_wrow(int wn, int b) {
+  if (EPI == EPI_SWIGLU) {
+    constexpr int HALF_W = BN / 2 / WGN;
+    return (b < FN / 2) ? wn * HALF_W + b * 32 : BN / 2 + wn * HALF_W + (b - FN / 2) * 32;
+  }
+  return wn * (BN / WGN) + b * 32;
+}
+
+// Store one wave's FM x FN accumulator fragments of tile t.  Lane holds token row
+// trow + astride a + (lane & 31) and output features fcol + 32 b + 8 q + 4 (lane >> 5) + 0..3.
+// SwiGLU pairs fragment b (gate) with b + FN/2 (up): Y = bf16(silu(gate) * up).
+template <int EPI, int FM, int FN>
+__device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&acc)[FM][FN], const TileDesc& t,
+                                           int trow, int astride, int fcol, int lane) {
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    const int row = t.row0 + trow + a * astride + (lane & 31);
+    if (row >= t.row_end) continue;
+    if (EPI == EPI_SWIGLU) {
+      bf16_t* yrow = reinterpret_cast<bf16_t*>(t.Y) + (int64_t)row * p.ldy;
+#pragma unroll
+      for (int b = 0; b < FN / 2; ++b) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int col = fcol + b * 32 + 8 * q + 4 * (lane >> 5);
+          if (col >= p.N) continue;
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float gt = acc[a][b][4 * q + e], up = acc[a][b + FN / 2][4 * q + e];
+            o[e] = gt / (1.0f + __expf(-gt)) * up;
+          }
+          uint2 v;
+          v.x = pack_bf16x2(o[0], o[1]);
+          v.y = pack_bf16x2(o[2], o[3]);
+          *reinterpret_cast<uint2*>(yrow + col) = v;
+        }
+      }
+    } else if (EPI == EPI_BF16) {
+      bf16_t* yrow = reinterpret_cast<bf16_t*>(t.Y) + (int64_t)row * p.ldy;
+#pragma unroll
+      for (int b = 0; b < FN; ++b) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int col = fcol + b * 32 + 8 * q + 4 * (lane >> 5);
+          if (col >= p.N) continue;
+          uint2 v;
+          v.x = pack_bf16x2(acc[a][b][4 * q + 0], acc[a][b][4 * q + 1]);
+          v.y = pack_bf16x2(acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]);
+          *reinterpret_cast<uint2*>(yrow + col) = v;
+        }
+      }
+    } else {
+      float* yrow = reinterpret_cast<float*>(t.Y) + (int64_t)row * p.ldy;
+#pragma unroll
+      for (int b = 0; b < FN; ++b) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int col = fcol + b * 32 + 8 * q + 4 * (lane >> 5);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < p.N) yrow[col + e] = acc[a][b][4 * q + e];
+        }
+      }
+    }
+  }
+}
+
+// f(std::integral_constant<int, k>) with k = min(n, N) (n >= 0)
+template <int N, class F>
+__device__ __forceinline__ void with_count(int n, F&& f) {
+  if constexpr (N == 0) {
+    f(std::integral_constant<int, 0>{});
+  } else {
+    if (n >= N) f(std::integral_constant<int, N>{});
+    else with_count<N - 1>(n, f);
+  }
+}
+
+template <int FM, int FN>
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[FM][FN]) {
+#pragma unroll
+  for (int a = 0; a < FM; ++a)
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
+}
+
+// ---------------------------------------------------------------------------------------
+// The kernel: every wave copies, reads and multiplies
+// ---------------------------------------------------------------------------------------
+
+// BM token rows x BN weight rows per tile, WGM x WGN waves (each a (BM/WGM) x (BN/WGN)
+// sub-tile), BK-wide K slices through a STAGES-deep ring.
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem p) {
+  using Z = Swz<BK>;
+  constexpr int NW = WGM * WGN, NTH = 64 * NW;
+  constexpr int WM = BM / WGM, WN = BN / WGN;             // per-wave sub-tile
+  constexpr int FM = WM / 32, FN = WN / 32;               // 32x32 fragments per wave
+  constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
+  constexpr int SLICE = (BM + BN) * BK;                   // bf16 elements per ring slot
+  using CP = CopyPlan<BM, BN, BK, NW, EPI>;
+  constexpr int L = CP::L;
+  static_assert(FM >= 1 && FN >= 1, "tile too small");
+  static_assert(EPI != EPI_SWIGLU || (FN % 2 == 0 && (BN / 2 / WGN) % 32 == 0), "SwiGLU pairs gate and up fragments");
+  static_assert(STAGES >= 2 && (STAGES - 2) * L < 64, "ring depth");
+
+  extern __shared__ __align__(16) uint8_t smem[];
+  bf16_t* ring = reinterpret_cast<bf16_t*>(smem);         // [STAGES][BM + BN][BK]: X rows then W rows
+  __shared__ int s_off[kMaxGroups + 1];
+  __shared__ int s_tp[kMaxGroups + 1];
+  __shared__ int s_tmp[NTH / 64];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const TileSpace ts = build_tile_space<NTH, BM>(p, OUTN, s_off, s_tp, s_tmp);
+  const int G = gridDim.x;
+  const int K = p.K;
+  const int nk = (K + BK - 1) / BK;
   const int nk_full = K / BK;
+  constexpr bool ktail = KTAIL;                           // K % BK != 0 (launcher-checked)
+
+  CP cp;
   auto issue_any = [&](int kt, int st) {
     if constexpr (KTAIL) {
-      if (kt >= nk_full) issue_tail(kt, st);
-      else issue(kt, st);
+      if (kt >= nk_full) cp.issue_tail(ring + st * SLICE, kt, wave, K);
+      else cp.issue(ring + st * SLICE, kt, wave);
     } else {
-      issue(kt, st);
+      cp.issue(ring + st * SLICE, kt, wave);
     }
   };
 
@@ -322,155 +459,112 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     if (ktail && kt == nk - 1) {
       // zero the chunks past K of the last slice (their copies came from clamped addresses)
       bf16_t* z = ring + (kt % STAGES) * SLICE;
-      for (int idx = tid; idx < (BM + BN) * S::CPR; idx += NTH) {
-        const int r = idx / S::CPR, pc = idx % S::CPR;
-        const int c = pc ^ S::f(r);
+      for (int idx = tid; idx < (BM + BN) * Z::CPR; idx += NTH) {
+        const int r = idx / Z::CPR, pc = idx % Z::CPR;
+        const int c = pc ^ Z::f(r);
         if (kt * BK + c * 8 >= K) st16(z + r * BK + pc * 8, u32x4{0, 0, 0, 0});
       }
       lds_barrier();
     }
   };
 
-  // per-lane LDS element offsets of this wave's fragment rows (chunk 0 of the row)
+  // Token rows: fragment a of wave (wm, wn) holds the tile's 32-row block a * WGM + wm, so the
+  // row blocks alternate over the waves.  A tile whose segment ends early (the ragged last
+  // m-tile of a group) leaves every wave with fewer live blocks; a wave multiplies only its
+  // live ones (NA of FM, uniform per wave and tile), and the blocks past the end cost no MFMA.
   constexpr int KS = BK / 16;                             // MFMA K-steps per slice
   int wrow_l[FN], xrow_l[FM], wf_l[FN], xf_l[FM];
 #pragma unroll
   for (int b = 0; b < FN; ++b) {
-    const int r = wbase[b] + (lane & 31);
+    const int r = frag_wrow<EPI, BN, WGN, FN>(wn, b) + (lane & 31);
     wrow_l[b] = BM * BK + r * BK;
-    wf_l[b] = S::f(r);
+    wf_l[b] = Z::f(r);
   }
 #pragma unroll
   for (int a = 0; a < FM; ++a) {
-    const int r = wm * WM + a * 32 + (lane & 31);
+    const int r = (a * WGM + wm) * 32 + (lane & 31);
     xrow_l[a] = r * BK;
-    xf_l[a] = S::f(r);
+    xf_l[a] = Z::f(r);
   }
   const int hi = lane >> 5;
   bf16x8 fw[2][FN], fx[2][FM];
-  auto load_frags = [&](int buf, int st, int ks) {
+  // read the fragments of K-step ks of ring slot st (the first NA token fragments)
+  auto load_frags = [&](auto na, int buf, int st, int ks) {
+    constexpr int NA = decltype(na)::value;
     const bf16_t* base = ring + st * SLICE;
     const int c = ks * 2 + hi;
+    if constexpr (NA > 0) {
 #pragma unroll
-    for (int b = 0; b < FN; ++b)
-      fw[buf][b] = *reinterpret_cast<const bf16x8*>(base + wrow_l[b] + ((c ^ wf_l[b]) << 3));
+      for (int b = 0; b < FN; ++b)
+        fw[buf][b] = *reinterpret_cast<const bf16x8*>(base + wrow_l[b] + ((c ^ wf_l[b]) << 3));
 #pragma unroll
-    for (int a = 0; a < FM; ++a)
-      fx[buf][a] = *reinterpret_cast<const bf16x8*>(base + xrow_l[a] + ((c ^ xf_l[a]) << 3));
+      for (int a = 0; a < NA; ++a)
+        fx[buf][a] = *reinterpret_cast<const bf16x8*>(base + xrow_l[a] + ((c ^ xf_l[a]) << 3));
+    }
   };
 
-  int tile = slot;
-  if (tile >= total) return;
-  int row0, row_end, ni;
-  setup_tile(tile, row0, row_end, ni);
+  int tile = first_tile_slot();
+  if (tile >= ts.total) return;
+  TileDesc td = decode_tile<BM>(p, ts, tile);
+  cp.setup(p, td, wave, lane);
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue_any(s, s);
 
+  const int fcol = (EPI == EPI_SWIGLU ? wn * (BN / 2 / WGN) : wn * WN);
   while (true) {
     f32x16 acc[FM][FN];
-#pragma unroll
-    for (int a = 0; a < FM; ++a)
-#pragma unroll
-      for (int b = 0; b < FN; ++b)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
+    zero_acc(acc);
 
-    sync_slice(0);
-    load_frags(0, 0, 0);
-    for (int kt = 0; kt < nk; ++kt) {
-      const int st = kt % STAGES;
+    // the K loop of one tile with NA live token fragments
+    auto k_loop = [&](auto na) {
+      constexpr int NA = decltype(na)::value;
+      sync_slice(0);
+      load_frags(na, 0, 0, 0);
+      for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt % STAGES;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int cur = ks & 1;
-        if (ks + 1 < KS) {
-          load_frags(cur ^ 1, st, ks + 1);
-        } else {
-          // the last step's fragments are in registers: publish the next slice now, so the
-          // barrier and the first reads of the next slice overlap this step's MFMAs (after
-          // the final slice this reads a stale ring slot, harmlessly, to keep the loop
-          // free of branches the wait-count insertion would have to merge)
-          sync_slice(kt + 1);
-          load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
+        for (int ks = 0; ks < KS; ++ks) {
+          const int cur = ks & 1;
+          if (ks + 1 < KS) {
+            load_frags(na, cur ^ 1, st, ks + 1);
+          } else {
+            // the last step's fragments are in registers: publish the next slice now, so the
+            // barrier and the first reads of the next slice overlap this step's MFMAs (after
+            // the final slice this reads a stale ring slot, harmlessly, to keep the loop
+            // free of branches the wait-count insertion would have to merge)
+            sync_slice(kt + 1);
+            load_frags(na, cur ^ 1, (kt + 1) % STAGES, 0);
+          }
+#pragma unroll
+          for (int a = 0; a < NA; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+          // scheduling: an MFMA first (its operands were read during the previous step), then
+          // the next step's LDS reads two at a time between MFMAs, so every read has several
+          // MFMAs of this step to hide its latency behind
+          if constexpr (NA > 0) sched_step<NA + FN, NA * FN>();
         }
-#pragma unroll
-        for (int a = 0; a < FM; ++a)
-#pragma unroll
-          for (int b = 0; b < FN; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
-        // scheduling: an MFMA first (its operands were read during the previous step), then
-        // the next step's LDS reads two at a time between MFMAs, so every read has several
-        // MFMAs of this step to hide its latency behind
-        sched_step<FM + FN, FM * FN>();
       }
-    }
+    };
+    const int live_blocks = min(BM / 32, (td.row_end - td.row0 + 31) / 32);
+    const int na = __builtin_amdgcn_readfirstlane(max(0, (live_blocks - wm + WGM - 1) / WGM));
+    with_count<FM>(na, k_loop);
 
     // next tile: start its copies before this tile's epilogue (every wave is done with the ring)
-    const int c_row0 = row0, c_row_end = row_end, c_ni = ni;
-    void* const c_y = ytile;
+    const TileDesc cur_td = td;
     tile += G;
-    const bool more = tile < total;
+    const bool more = tile < ts.total;
     lds_barrier();
     if (more) {
-      setup_tile(tile, row0, row_end, ni);
+      td = decode_tile<BM>(p, ts, tile);
+      cp.setup(p, td, wave, lane);
 #pragma unroll
       for (int s = 0; s < STAGES - 1; ++s)
         if (s < nk) issue_any(s, s);
     }
-
-    // ---- epilogue: lane holds token column (lane & 31); features 8q + 4(lane>>5) + 0..3 ----
-#pragma unroll
-    for (int a = 0; a < FM; ++a) {
-      const int row = c_row0 + wm * WM + a * 32 + (lane & 31);
-      if (row >= c_row_end) continue;
-      if (EPI == EPI_SWIGLU) {
-        bf16_t* yrow = reinterpret_cast<bf16_t*>(c_y) + (int64_t)row * p.ldy;
-#pragma unroll
-        for (int b = 0; b < FN / 2; ++b) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = c_ni * (BN / 2) + wn * HALF_W + b * 32 + 8 * q + 4 * (lane >> 5);
-            if (col >= p.N) continue;
-            float o[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              float gt = acc[a][b][4 * q + e], up = acc[a][b + FN / 2][4 * q + e];
-              o[e] = gt / (1.0f + __expf(-gt)) * up;
-            }
-            uint2 v;
-            v.x = pack_bf16x2(o[0], o[1]);
-            v.y = pack_bf16x2(o[2], o[3]);
-            *reinterpret_cast<uint2*>(yrow + col) = v;
-          }
-        }
-      } else if (EPI == EPI_BF16) {
-        bf16_t* yrow = reinterpret_cast<bf16_t*>(c_y) + (int64_t)row * p.ldy;
-#pragma unroll
-        for (int b = 0; b < FN; ++b) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = c_ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
-            if (col >= p.N) continue;
-            uint2 v;
-            v.x = pack_bf16x2(acc[a][b][4 * q + 0], acc[a][b][4 * q + 1]);
-            v.y = pack_bf16x2(acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]);
-            *reinterpret_cast<uint2*>(yrow + col) = v;
-          }
-        }
-      } else {
-        float* yrow = reinterpret_cast<float*>(c_y) + (int64_t)row * p.ldy;
-#pragma unroll
-        for (int b = 0; b < FN; ++b) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int col = c_ni * BN + wn * WN + b * 32 + 8 * q + 4 * (lane >> 5);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (col + e < p.N) yrow[col + e] = acc[a][b][4 * q + e];
-          }
-        }
-      }
-    }
+    store_tile<EPI, FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane);
     if (!more) break;
   }
 }
@@ -499,34 +593,42 @@ DevInfo& dev_info() {
 int cu_count() { return dev_info().cus; }
 int lds_limit() { return dev_info().lds; }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
-hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
-  constexpr int NTH = 64 * WGM * WGN;
-  constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
-  const void* fn = reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>);
-  const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t);
+// Persistent launch of kernel `fn` (nth threads, lds bytes of dynamic LDS): grid = the
+// smaller of an upper bound of the launch's tile count and the resident workgroups, rounded
+// down to whole rounds of the 8 XCDs.  per_cu caches the kernel's occupancy (idempotent;
+// racing writers store the same value).
+hipError_t launch_persistent(const void* fn, int& per_cu, int nth, size_t lds, int bm, int outn,
+                             const GemmProblem& p, hipStream_t stream) {
   const size_t lds_static = 2 * (kMaxGroups + 1) * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
-  static int per_cu = 0;   // resident workgroups per CU (idempotent; racing writers store the same value)
   if (per_cu == 0) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     int occ = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, NTH, lds);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, nth, lds);
     if (e != hipSuccess) return e;
     per_cu = occ > 0 ? occ : 1;
   }
-  const int64_t tiles_n = (p.N + OUTN - 1) / OUTN;
+  const int64_t tiles_n = (p.N + outn - 1) / outn;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
-  const int64_t upper = tiles_n * ((rows + BM - 1) / BM + groups + (p.rows2 + BM - 1) / BM);
+  const int64_t upper = tiles_n * ((rows + bm - 1) / bm + groups + (p.rows2 + bm - 1) / bm);
   const int64_t resident = (int64_t)cu_count() * per_cu;
   int64_t grid = upper < resident ? upper : resident;
   if (grid >= 8) grid -= grid % 8;
   if (grid < 1) grid = 1;
-  hipLaunchKernelGGL((k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>), dim3((unsigned)grid), dim3(NTH),
-                     lds, stream, p);
-  return hipGetLastError();
+  GemmProblem arg = p;
+  void* args[] = {&arg};
+  hipError_t e = hipLaunchKernel(fn, dim3((unsigned)grid), dim3(nth), args, lds, stream);
+  return e != hipSuccess ? e : hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
+hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
+  static int per_cu = 0;
+  const void* fn = reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>);
+  return launch_persistent(fn, per_cu, 64 * WGM * WGN, (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t), BM,
+                           EPI == EPI_SWIGLU ? BN / 2 : BN, p, stream);
 }
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI>

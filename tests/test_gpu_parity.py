@@ -233,3 +233,33 @@ def test_full_workload_parity(name):
     print(f"[parity] {name}: rel_fro={err:.3e} on {toks.size} tokens, near_ties={len(near)}, local rows={n}, "
           f"counts min/median/max={cnt.min()}/{int(np.median(cnt))}/{cnt.max()}", flush=True)
     assert err <= REL_TOL
+
+
+def test_grouped_ffn_ragged_tail_blocks():
+    """moe_grouped_ffn on hand-picked segment lengths: the last m-tile of a segment holds every
+    count of live 32-row blocks (1 .. 8, block edges +-1), plus empty segments, multi-tile
+    segments and K tails in both GEMMs (d = 264, F = 136); each segment against the oracle."""
+    lengths = [1, 0, 31, 32, 33, 63, 64, 65, 96, 127, 128, 129, 160, 191, 224, 255, 256, 0, 273, 612]
+    E = len(lengths)
+    T = int(sum(lengths))
+    sh = S(T=T, d=264, E=E, top_k=1, F=136, E_local=E)
+    rng = np.random.default_rng(2024)
+    x = wl.f32_to_bf16_bits(rng.standard_normal((T, sh.d)).astype(np.float32))
+    w13 = wl.f32_to_bf16_bits((rng.standard_normal((E, 2 * sh.F, sh.d)) * sh.d ** -0.5).astype(np.float32))
+    w2 = wl.f32_to_bf16_bits((rng.standard_normal((E, sh.d, sh.F)) * sh.F ** -0.5).astype(np.float32))
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    dev = "cuda"
+    y = torch.full((sh.capacity, sh.d), float("nan"), dtype=torch.bfloat16, device=dev)
+    moe.moe_grouped_ffn(sh, moe.to_device_bf16(x), torch.from_numpy(offs).to(dev), moe.to_device_bf16(w13),
+                        moe.to_device_bf16(w2), y, moe.alloc_workspace(sh, moe.MOE_WS_FFN))
+    torch.cuda.synchronize()
+    got = y.float().cpu().numpy()
+    assert np.isfinite(got[:T]).all()
+    xd = oracle.bf16_to_f64(x)
+    for e in range(E):
+        a, b = offs[e], offs[e + 1]
+        if a == b:
+            continue
+        ref = oracle.swiglu_ffn(xd[a:b], oracle.bf16_to_f64(w13[e]), oracle.bf16_to_f64(w2[e]))
+        err = rel_fro(got[a:b], ref)
+        assert err <= REL_TOL, (e, lengths[e], err)
