@@ -89,7 +89,10 @@ int check_ptr(const void* p, size_t align, const char* name) {
   } while (0)
 
 // ---- workspace layouts ----
-size_t ws_route(const moe_shape_t* s) { return align_up((size_t)s->T * s->E * sizeof(float)); }
+// router logits: one [T, E] fp32 partial per K chunk of the logits GEMM
+size_t ws_route(const moe_shape_t* s) {
+  return align_up((size_t)moe::logits_splits(s->T, s->E, s->d) * s->T * s->E * sizeof(float));
+}
 size_t ws_permute(const moe_shape_t* s) {
   return 2 * align_up((size_t)moe::permute_blocks(s->T) * s->E_local * sizeof(int32_t));
 }
@@ -181,10 +184,15 @@ int do_route(const moe_shape_t* s, const void* x, const void* w_router, const fl
   g.Y = logits;
   g.ldy = s->E;
   g.epi = moe::EPI_F32;
+  const int splits = moe::logits_splits(s->T, s->E, s->d);
+  g.ksplit = splits;
+  g.y_split_stride = s->T * (int64_t)s->E;
   CHECK(hip_status(moe::launch_grouped_gemm(g, st), "router logits launch"));
   if (mark) CHECK(mark(MOE_STEP_GATE));
   moe::GateProblem q{};
   q.logits = logits;
+  q.nsplit = splits;
+  q.split_stride = s->T * (int64_t)s->E;
   q.bias = bias;
   q.T = s->T;
   q.E = s->E;

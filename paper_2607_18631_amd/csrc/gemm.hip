@@ -123,14 +123,19 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
 
 // Tiles of one launch: `groups` row segments of BM-row tiles x tiles_n output tiles each,
 // plus tiles_x tiles of the optional extra group, `total` in all.  s_off / s_tp live in LDS.
+// With a K split (ksplit > 1, one group, no extra group) the tile space is ksplit copies of
+// the (m, n) tiles, chunk c covering K slices [c * kchunk, min(nk, (c + 1) * kchunk)); chunk is
+// the slowest index, so the workgroups of one XCD work on one K chunk of the weights.
 struct TileSpace {
   int groups, tiles_n, tiles_x, total;
+  int base_total;            // (m, n) tiles
+  int nk, kchunk;            // K slices; slices per chunk
   const int* s_off;          // [groups + 1] row offsets clamped to [0, max_rows]
   const int* s_tp;           // [groups + 1] first tile of each group; s_tp[groups] = grouped tiles
 };
 
 // Build the launch's tile table in LDS (every thread of the block calls this).
-template <int NTH, int BM>
+template <int NTH, int BM, int BK>
 __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off, int* s_tp, int* s_tmp) {
   const int tid = threadIdx.x;
   TileSpace ts;
@@ -169,7 +174,11 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
   // tile iff floor((t+1) S / total) > floor(t S / total)), so HBM-bound expert tiles and
   // compute-bound shared-expert tiles run side by side
   ts.tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * ts.tiles_n : 0;
-  ts.total = total_r + ts.tiles_x;
+  ts.base_total = total_r + ts.tiles_x;
+  ts.nk = (p.K + BK - 1) / BK;
+  const int ksplit = p.ksplit > 1 ? p.ksplit : 1;
+  ts.kchunk = (ts.nk + ksplit - 1) / ksplit;
+  ts.total = ts.base_total * ksplit;
   ts.groups = groups;
   ts.s_off = s_off;
   ts.s_tp = s_tp;
@@ -186,6 +195,7 @@ __device__ __forceinline__ int first_tile_slot() {
 // of the weights W, results into Y.
 struct TileDesc {
   int row0, row_end, ni;
+  int kb, ke, kc;            // K slices [kb, ke) of K chunk kc
   const bf16_t* X;
   const bf16_t* W;
   void* Y;
@@ -194,8 +204,12 @@ struct TileDesc {
 template <int BM>
 __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const TileSpace& ts, int tile) {
   TileDesc d;
-  const int x_before = (int)((int64_t)tile * ts.tiles_x / ts.total);
-  const bool extra = (int)((int64_t)(tile + 1) * ts.tiles_x / ts.total) > x_before;
+  d.kc = tile / ts.base_total;
+  tile -= d.kc * ts.base_total;
+  d.kb = d.kc * ts.kchunk;
+  d.ke = min(ts.nk, d.kb + ts.kchunk);
+  const int x_before = (int)((int64_t)tile * ts.tiles_x / ts.base_total);
+  const bool extra = (int)((int64_t)(tile + 1) * ts.tiles_x / ts.base_total) > x_before;
   int row0g, local;
   if (extra) {
     row0g = 0;
@@ -365,15 +379,21 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
         }
       }
     } else {
-      float* yrow = reinterpret_cast<float*>(t.Y) + (int64_t)row * p.ldy;
+      float* yrow = reinterpret_cast<float*>(t.Y) + t.kc * p.y_split_stride + (int64_t)row * p.ldy;
+      const bool vec = (p.ldy % 4 == 0) && (p.y_split_stride % 4 == 0);   // 16-byte aligned rows
 #pragma unroll
       for (int b = 0; b < FN; ++b) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int col = fcol + b * 32 + 8 * q + 4 * (lane >> 5);
+          if (vec && col + 3 < p.N) {
+            const f32x4 v = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]};
+            *reinterpret_cast<f32x4*>(yrow + col) = v;
+          } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (col + e < p.N) yrow[col + e] = acc[a][b][4 * q + e];
+            for (int e = 0; e < 4; ++e)
+              if (col + e < p.N) yrow[col + e] = acc[a][b][4 * q + e];
+          }
         }
       }
     }
@@ -430,7 +450,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
-  const TileSpace ts = build_tile_space<NTH, BM>(p, OUTN, s_off, s_tp, s_tmp);
+  const TileSpace ts = build_tile_space<NTH, BM, BK>(p, OUTN, s_off, s_tp, s_tmp);
   const int G = gridDim.x;
   const int K = p.K;
   const int nk = (K + BK - 1) / BK;
@@ -447,18 +467,21 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     }
   };
 
-  // make slice kt readable by every wave and refill the ring slot that slice kt-1 used
-  // (kt may be nk: then it only waits for every copy and synchronises)
-  auto sync_slice = [&](int kt) {
-    const int after = min(STAGES - 2, nk - 1 - kt);      // slices issued after kt
+  // The current tile runs K slices kb .. kb + nl - 1; its i-th slice lives in ring slot
+  // i % STAGES.  sync_slice(i) makes slice i readable by every wave and refills the ring slot
+  // that slice i-1 used (i may be nl: then it only waits for every copy and synchronises).
+  int kb = 0, nl = nk;
+  auto sync_slice = [&](int i) {
+    const int after = min(STAGES - 2, nl - 1 - i);       // slices issued after i
     if (STAGES >= 4 && after >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * L : 0)>();
     else if (STAGES >= 3 && after >= 1) wait_vmcnt<(STAGES >= 3 ? L : 0)>();
     else wait_vmcnt<0>();
     lds_barrier();
-    if (kt + STAGES - 1 < nk) issue_any(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    if (ktail && kt == nk - 1) {
+    if (i + STAGES - 1 < nl) issue_any(kb + i + STAGES - 1, (i + STAGES - 1) % STAGES);
+    const int kt = kb + i;
+    if (ktail && i < nl && kt == nk - 1) {
       // zero the chunks past K of the last slice (their copies came from clamped addresses)
-      bf16_t* z = ring + (kt % STAGES) * SLICE;
+      bf16_t* z = ring + (i % STAGES) * SLICE;
       for (int idx = tid; idx < (BM + BN) * Z::CPR; idx += NTH) {
         const int r = idx / Z::CPR, pc = idx % Z::CPR;
         const int c = pc ^ Z::f(r);
@@ -507,9 +530,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   if (tile >= ts.total) return;
   TileDesc td = decode_tile<BM>(p, ts, tile);
   cp.setup(p, td, wave, lane);
+  kb = td.kb;
+  nl = td.ke - td.kb;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue_any(s, s);
+    if (s < nl) issue_any(kb + s, s);
 
   const int fcol = (EPI == EPI_SWIGLU ? wn * (BN / 2 / WGN) : wn * WN);
   while (true) {
@@ -521,8 +546,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       constexpr int NA = decltype(na)::value;
       sync_slice(0);
       load_frags(na, 0, 0, 0);
-      for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt % STAGES;
+      for (int i = 0; i < nl; ++i) {
+        const int st = i % STAGES;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int cur = ks & 1;
@@ -533,8 +558,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
             // barrier and the first reads of the next slice overlap this step's MFMAs (after
             // the final slice this reads a stale ring slot, harmlessly, to keep the loop
             // free of branches the wait-count insertion would have to merge)
-            sync_slice(kt + 1);
-            load_frags(na, cur ^ 1, (kt + 1) % STAGES, 0);
+            sync_slice(i + 1);
+            load_frags(na, cur ^ 1, (i + 1) % STAGES, 0);
           }
 #pragma unroll
           for (int a = 0; a < NA; ++a)
@@ -560,9 +585,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     if (more) {
       td = decode_tile<BM>(p, ts, tile);
       cp.setup(p, td, wave, lane);
+      kb = td.kb;
+      nl = td.ke - td.kb;
 #pragma unroll
       for (int s = 0; s < STAGES - 1; ++s)
-        if (s < nk) issue_any(s, s);
+        if (s < nl) issue_any(kb + s, s);
     }
     store_tile<EPI, FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane);
     if (!more) break;
@@ -612,7 +639,8 @@ hipError_t launch_persistent(const void* fn, int& per_cu, int nth, size_t lds, i
   const int64_t tiles_n = (p.N + outn - 1) / outn;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
-  const int64_t upper = tiles_n * ((rows + bm - 1) / bm + groups + (p.rows2 + bm - 1) / bm);
+  const int64_t upper = tiles_n * ((rows + bm - 1) / bm + groups + (p.rows2 + bm - 1) / bm) *
+                        (p.ksplit > 1 ? p.ksplit : 1);
   const int64_t resident = (int64_t)cu_count() * per_cu;
   int64_t grid = upper < resident ? upper : resident;
   if (grid >= 8) grid -= grid % 8;
@@ -649,17 +677,69 @@ hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
     case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI>(p, stream);
     case 6: return launch_tile<256, 256, 64, 2, 4, 2, EPI>(p, stream);
     case 7: return launch_tile<256, 128, 64, 3, 4, 2, EPI>(p, stream);
-    default: return hipErrorInvalidValue;
+#ifdef MOE_GEMM_SWEEP
+    // narrow-N shapes (router logits, fp32 epilogue)
+    case 13: if constexpr (EPI == EPI_F32) return launch_tile<64, 64, 64, 3, 2, 2, EPI>(p, stream); break;
+    case 14: if constexpr (EPI == EPI_F32) return launch_tile<64, 128, 64, 3, 2, 2, EPI>(p, stream); break;
+    case 15: if constexpr (EPI == EPI_F32) return launch_tile<128, 64, 64, 3, 2, 2, EPI>(p, stream); break;
+    case 16: if constexpr (EPI == EPI_F32) return launch_tile<32, 256, 64, 3, 1, 4, EPI>(p, stream); break;
+    case 17: if constexpr (EPI == EPI_F32) return launch_tile<64, 256, 64, 2, 2, 4, EPI>(p, stream); break;
+    case 18: if constexpr (EPI == EPI_F32) return launch_tile<128, 128, 64, 2, 4, 2, EPI>(p, stream); break;
+    case 19: if constexpr (EPI == EPI_F32) return launch_tile<64, 64, 128, 2, 2, 2, EPI>(p, stream); break;
+#endif
+    default: break;
   }
+  return hipErrorInvalidValue;
 }
 
 #ifdef MOE_GEMM_SWEEP
 int g_force_cfg[3] = {-1, -1, -1};
 #endif
 
+// (BM, BN, BK) of the tile the fp32-output GEMM runs with: the 256 x 256 tile (K-split for
+// parallelism) when there are many tokens and experts, else 64 x 64 tiles
+struct TileShape {
+  int bm, bn, bk;
+};
+bool f32_big_tile(int64_t rows, int n) { return rows >= 4096 && n >= 128; }
+TileShape f32_tile(int64_t rows, int n) {
+#ifdef MOE_GEMM_SWEEP
+  switch (g_force_cfg[EPI_F32]) {
+    case 0: return {128, 128, 64};
+    case 6: return {256, 256, 64};
+    case 13: return {64, 64, 64};
+    case 14: return {64, 128, 64};
+    case 15: return {128, 64, 64};
+    case 16: return {32, 256, 64};
+    case 17: return {64, 256, 64};
+    case 18: return {128, 128, 64};
+    case 19: return {64, 64, 128};
+    default: break;
+  }
+#endif
+  if (f32_big_tile(rows, n)) return {256, 256, 64};
+  return {64, 64, 64};
+}
+
 }  // namespace
 
+int logits_splits(int64_t T, int E, int K) {
+  constexpr int64_t kTarget = 256;                         // compute units of an MI355X
+  constexpr int64_t kMaxSplits = 16;                       // bounds the partials the gate adds
+  const TileShape t = f32_tile(T, E);
+  const int64_t base = ((T + t.bm - 1) / t.bm) * ((E + t.bn - 1) / t.bn);
+  const int64_t nk = (K + t.bk - 1) / t.bk;
+  if (base <= 0 || nk <= 1) return 1;
+  int64_t s = (kTarget + base - 1) / base;
+  s = s < nk ? s : nk;
+  s = s < kMaxSplits ? s : kMaxSplits;
+  if (s <= 1) return 1;
+  const int64_t chunk = (nk + s - 1) / s;
+  return (int)((nk + chunk - 1) / chunk);                // every chunk non-empty
+}
+
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
+  if (p.ksplit > 1 && (p.epi != EPI_F32 || p.offsets != nullptr || p.rows2 > 0)) return hipErrorInvalidValue;
   // 256 x 256 tiles, 8 waves, two 64-wide K slices in flight: the best measured on the DeepSeek-V3,
   // Mixtral and skewed workloads (largest reuse per byte copied into LDS)
   int cfg_swiglu = 6, cfg_bf16 = 6;
@@ -670,7 +750,13 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   switch (p.epi) {
     case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
     case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
-    case EPI_F32: return launch_tile<64, 64, 64, 3, 2, 2, EPI_F32>(p, stream);
+    case EPI_F32:
+#ifdef MOE_GEMM_SWEEP
+      if (g_force_cfg[EPI_F32] >= 0) return launch_cfg<EPI_F32>(g_force_cfg[EPI_F32], p, stream);
+#endif
+      if (f32_big_tile(p.offsets ? p.max_rows : p.rows_single, p.N))
+        return launch_tile<256, 256, 64, 2, 4, 2, EPI_F32>(p, stream);
+      return launch_tile<64, 64, 64, 3, 2, 2, EPI_F32>(p, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -35,12 +35,23 @@ struct GemmProblem {
   const bf16_t* W2;
   void* Y2;
   int32_t rows2;
+  // K split (EPI_F32, one group, no extra group): ksplit > 1 runs the K range in ksplit
+  // chunks, chunk c writing its fp32 partial product at Y + c * y_split_stride
+  int32_t ksplit;
+  int64_t y_split_stride;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
 
+// Number of K chunks the router-logits GEMM (T x E outputs, K = d) runs in: enough (m, n, k)
+// tiles for one per compute unit of the chip, every chunk non-empty.  Depends on the shape
+// only, so workspace sizes do not depend on the device.
+int logits_splits(int64_t T, int E, int K);
+
 struct GateProblem {
-  const float* logits;        // [T, E]
+  const float* logits;        // nsplit partial sums, each [T, E]: logits = sum of the partials
+  int32_t nsplit;
+  int64_t split_stride;       // elements between partials
   const float* bias;          // [E] or nullptr
   int64_t T;
   int32_t E, top_k, gate, n_group, topk_group, renormalize;

@@ -6,7 +6,7 @@
 //                  the expert total (counts[e])
 //   k_rank         per chunk: the offsets (exclusive scan of counts, the monotone
 //                  [E_local+1] array), each slot's rank among the chunk's earlier slots
-//                  of the same expert, hence its row
+//                  of the same expert (slot columns spread over the waves), hence its row
 //                      row = offsets[e] + chunk_base[c][e] + rank,
 //                  then row_token / slot_row
 //   k_gather       per token: the bit-exact copy of the token row to each of its local
@@ -71,18 +71,20 @@ __global__ __launch_bounds__(256) void k_chunk_scan(PermuteProblem p, int nblk) 
   if (tid == 0) p.counts[e] = carry;
 }
 
-// one workgroup per chunk: offsets (every workgroup; workgroup 0 publishes them), then wave 0
-// ranks the chunk's slots and writes row_token / slot_row
-__global__ __launch_bounds__(256) void k_rank(PermuteProblem p) {
+// one workgroup per chunk: offsets (every workgroup; workgroup 0 publishes them), then the
+// chunk's slots are ranked, wave w taking slot columns w, w + RW, ... (every wave forms the
+// ballots of all columns, which are cheap; the per-slot rank work is split)
+constexpr int RW = 8;                          // waves of the rank kernel
+__global__ __launch_bounds__(64 * RW) void k_rank(PermuteProblem p) {
   extern __shared__ int s_off[];               // [E_local + 1]
-  __shared__ int s_w[4];
+  __shared__ int s_w[RW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = blockIdx.x;
   const int E_local = p.E_local, k = p.top_k;
 
   // offsets = exclusive scan of counts
   {
-    constexpr int PER = 4;                     // 256 threads x 4 >= 1024 experts
+    constexpr int PER = (1024 + 64 * RW - 1) / (64 * RW);   // threads x PER >= 1024 experts
     int v[PER], lsum = 0;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(256) void k_rank(PermuteProblem p) {
     __syncthreads();
     int run = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < RW; ++w) {
       if (w < wave) run += s_w[w];
       tot += s_w[w];
     }
@@ -114,28 +116,30 @@ __global__ __launch_bounds__(256) void k_rank(PermuteProblem p) {
     if (tid == 0) s_off[E_local] = tot;
     __syncthreads();
     if (c == 0)
-      for (int e = tid; e <= E_local; e += 256) p.offsets[e] = s_off[e];
+      for (int e = tid; e <= E_local; e += 64 * RW) p.offsets[e] = s_off[e];
   }
-  if (wave != 0) return;
+  if (wave >= k) return;                       // wave-uniform
 
-  // rank of each slot among the chunk's earlier slots of the same expert
+  // rank of each of my slots among the chunk's earlier slots of the same expert
   const int64_t t = (int64_t)c * CH + lane;
   const bool valid_t = t < p.T;
   int nbits = 0;
   while ((1 << nbits) < E_local) ++nbits;
   const int32_t* base = p.blk_base + (int64_t)c * E_local;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  constexpr int MINE = (16 + RW - 1) / RW;     // slot columns per wave (top_k <= 16)
   int myle[16];
-  int rank[16];
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     myle[j] = -1;
-    rank[j] = 0;
     if (j < k && valid_t) {
       const int le = p.topk_idx[t * k + j] - p.e_begin;
       myle[j] = (le >= 0 && le < E_local) ? le : -1;
     }
   }
+  int rank[MINE];
+#pragma unroll
+  for (int m = 0; m < MINE; ++m) rank[m] = 0;
 #pragma unroll
   for (int jp = 0; jp < 16; ++jp) {
     if (jp >= k) break;
@@ -146,22 +150,24 @@ __global__ __launch_bounds__(256) void k_rank(PermuteProblem p) {
 #pragma unroll
     for (int b = 0; b < 10; ++b) bal[b] = (b < nbits) ? __ballot(lej >= 0 && ((lej >> b) & 1)) : 0ull;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int m = 0; m < MINE; ++m) {
+      const int j = wave + m * RW;
       if (j >= k) break;
       const int le = myle[j];
-      uint64_t m = vmask;
+      uint64_t msk = vmask;
 #pragma unroll
       for (int b = 0; b < 10; ++b)
-        if (b < nbits) m &= ((le >> b) & 1) ? bal[b] : ~bal[b];
-      rank[j] += __popcll(m & below);
+        if (b < nbits) msk &= ((le >> b) & 1) ? bal[b] : ~bal[b];
+      rank[m] += __popcll(msk & below);
     }
   }
   if (!valid_t) return;
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
+  for (int m = 0; m < MINE; ++m) {
+    const int j = wave + m * RW;
     if (j >= k) break;
     int row = -1;
-    if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[j];
+    if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[m];
     if (row >= p.cap) row = -1;              // unreachable for a consistent histogram; keeps writes in bounds
     p.slot_row[t * k + j] = row;
     if (row >= 0) p.row_token[row] = (int32_t)t;
@@ -220,7 +226,7 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*bet
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (between && between() != 0) return hipErrorUnknown;
-  hipLaunchKernelGGL(k_rank, dim3((unsigned)nblk), dim3(256), (p.E_local + 1) * sizeof(int), stream, p);
+  hipLaunchKernelGGL(k_rank, dim3((unsigned)nblk), dim3(64 * RW), (p.E_local + 1) * sizeof(int), stream, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gather, dim3((unsigned)((p.T + 3) / 4)), dim3(256), 0, stream, p);

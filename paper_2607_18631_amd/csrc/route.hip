@@ -1,13 +1,20 @@
 // Gating and top-k: one wavefront per token.
 //
-// The router logits come from the grouped GEMM (one group, float32 epilogue).  Lane l of
-// the wave owns experts l, l + 64, l + 128, ... (up to 16 per lane for E <= 1024).  Every
-// decision is taken on the float32 key (softmax: logit + bias; sigmoid: the score), with
-// wave-wide butterfly argmax reductions: the larger key wins, equal keys go to the lower
-// expert index, so the result does not depend on lane scheduling.
+// The router logits come from the grouped GEMM (one group, float32 epilogue), possibly as
+// nsplit partial sums over K chunks; they are added here in chunk order.  Lane l of the wave
+// owns the PL contiguous experts [PL l, PL l + PL).  Every decision is taken on the float32
+// key (softmax: logit + bias; sigmoid: the score): the larger key wins, equal keys go to the
+// lower expert index, so the result does not depend on lane scheduling.
 //
-// Group limit (n_group > 1): each contiguous group scores the float32 sum of its two
-// largest keys (two argmax passes per group), the topk_group best groups stay eligible.
+// Wave-wide argmax: a (key, index) pair is packed into one 64-bit integer whose unsigned
+// order is (key ascending, index descending), so the pair to keep is the plain maximum.  The
+// maximum is taken with DPP moves inside each 16-lane row (no LDS traffic) and four lane reads
+// across the rows.
+//
+// Group limit (n_group > 1): the keys go through LDS; lane g scores group g (the float32 sum
+// of its two largest keys), ranks it against the other groups' scores (larger score first,
+// equal scores by lower group index), and a ballot of the ranks below topk_group is the mask
+// of eligible groups.
 #include <math.h>
 
 #include "common.hpp"
@@ -17,95 +24,224 @@ namespace moe {
 namespace {
 
 constexpr int kMaxPerLane = 16;   // E <= 1024
+constexpr int kWaves = 4;         // tokens per workgroup
+
+// float -> uint32 with the same order (finite values and infinities; -0 counts as +0)
+__device__ __forceinline__ uint32_t ordered(float f) {
+  const uint32_t u = __float_as_uint(f + 0.0f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t pack_key(float key, int idx) {
+  return ((uint64_t)ordered(key) << 32) | (uint32_t)(~(uint32_t)idx);
+}
+__device__ __forceinline__ int packed_index(uint64_t v) { return (int)~(uint32_t)v; }
+// the float key back from a packed pair (inverse of ordered)
+__device__ __forceinline__ float packed_key(uint64_t v) {
+  const uint32_t o = (uint32_t)(v >> 32);
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+
+// lanes of the rows in ROWS take src from the DPP pattern CTRL, the others keep their value
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)v, (int)(uint32_t)v, CTRL, ROWS, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(v >> 32), (int)(uint32_t)(v >> 32), CTRL, ROWS, 0xf, false);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// maximum over the 64 lanes, returned to every lane (wave-uniform)
+__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
+  v = umax64(v, dpp64<0xb1>(v));          // quad_perm [1,0,3,2]
+  v = umax64(v, dpp64<0x4e>(v));          // quad_perm [2,3,0,1]
+  v = umax64(v, dpp64<0x141>(v));         // row_half_mirror: quads 0 <-> 1 of each 8
+  v = umax64(v, dpp64<0x140>(v));         // row_mirror: halves of each 16-lane row
+  v = umax64(v, dpp64<0x142, 0xa>(v));    // row_bcast:15 -> rows 1, 3 hold rows (0,1), (2,3)
+  v = umax64(v, dpp64<0x143, 0xc>(v));    // row_bcast:31 -> row 3 holds all four
+  return readlane64(v, 63);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+// merge the two-largest multisets (v1 >= v2) of this lane and the DPP partner lane
+template <int CTRL>
+__device__ __forceinline__ void top2_merge(float& v1, float& v2) {
+  const float o1 = dppf<CTRL>(v1), o2 = dppf<CTRL>(v2);
+  v2 = fmaxf(fminf(v1, o1), fmaxf(v2, o2));
+  v1 = fmaxf(v1, o1);
+}
+// fixed-order sum / max over the 64 lanes (wave-uniform result)
+__device__ __forceinline__ float wave_sum_fixed(float v) {
+  v += dppf<0xb1>(v);
+  v += dppf<0x4e>(v);
+  v += dppf<0x141>(v);
+  v += dppf<0x140>(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+__device__ __forceinline__ float wave_max_fixed(float v) {
+  v = fmaxf(v, dppf<0xb1>(v));
+  v = fmaxf(v, dppf<0x4e>(v));
+  v = fmaxf(v, dppf<0x141>(v));
+  v = fmaxf(v, dppf<0x140>(v));
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
 
 template <int PL>
-__global__ __launch_bounds__(256) void k_gate(GateProblem p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= p.T) return;
+__global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
+  __shared__ float s_key[kWaves][64 * PL];
+  __shared__ float s_gscore[kWaves][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * kWaves + w;
+  if (t >= p.T) return;                                   // wave-uniform
   const int E = p.E;
   const float NEG = -INFINITY;
+  const int e0 = lane * PL;
 
-  float key[PL];
-  const float* lrow = p.logits + t * E;
+  // ---- logits (sum of the K-chunk partials, chunk order) and keys ----
+  // this lane's PL logits of one partial (16-byte loads where rows allow)
+  auto load_row = [&](const float* row, float (&v)[PL]) {
+    if constexpr (PL % 4 == 0) {
+      if (E % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < PL; ++i) {
-    const int e = i * 64 + lane;
+        for (int c = 0; c < PL / 4; ++c) {
+          f32x4 q = {0.f, 0.f, 0.f, 0.f};
+          if (e0 + 4 * c < E) q = *reinterpret_cast<const f32x4*>(row + e0 + 4 * c);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[4 * c + u] = q[u];
+        }
+        return;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < PL; ++j) v[j] = (e0 + j < E) ? row[e0 + j] : 0.f;
+  };
+  float key[PL];
+#pragma unroll
+  for (int j = 0; j < PL; ++j) key[j] = 0.f;
+  const float* row0 = p.logits + t * E;
+  int s = 0;
+  for (; s + 4 <= p.nsplit; s += 4) {                     // four partials' loads in flight
+    float v[4][PL];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load_row(row0 + (s + u) * p.split_stride, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < PL; ++j) key[j] += v[u][j];
+  }
+  for (; s < p.nsplit; ++s) {
+    float v[PL];
+    load_row(row0 + s * p.split_stride, v);
+#pragma unroll
+    for (int j = 0; j < PL; ++j) key[j] += v[j];
+  }
+#pragma unroll
+  for (int j = 0; j < PL; ++j) {
+    const int e = e0 + j;
     float k = NEG;
     if (e < E) {
-      const float L = lrow[e];
-      if (p.gate == 0) {
-        k = p.bias ? L + p.bias[e] : L;
-      } else {
-        k = 1.0f / (1.0f + expf(-L));
-      }
+      const float L = key[j];
+      k = (p.gate == 0) ? (p.bias ? L + p.bias[e] : L) : 1.0f / (1.0f + expf(-L));
       if (p.keys_out) p.keys_out[t * E + e] = k;
     }
-    key[i] = k;
+    key[j] = k;
   }
 
-  // ---- group limit: lane g holds the score of group g ----
-  bool elig[PL];
+  // ---- group limit ----
+  uint32_t elig = 0;                                      // bit j: expert e0 + j may be chosen
 #pragma unroll
-  for (int i = 0; i < PL; ++i) elig[i] = (i * 64 + lane) < E;
+  for (int j = 0; j < PL; ++j)
+    if (e0 + j < E) elig |= 1u << j;
   if (p.n_group > 1) {
-    const int gsz = E / p.n_group;
-    float my_gscore = NEG;
-    for (int g = 0; g < p.n_group; ++g) {
-      const int lo = g * gsz, hi = lo + gsz;
-      float v1 = NEG;
-      int i1 = 0x7fffffff;
+    const int ng = p.n_group, gsz = E / ng;
+    const int lpg = gsz / PL;                             // lanes per group when groups tile lanes
+    float gs = NEG;
+    if (gsz % PL == 0 && (lpg == 2 || lpg == 4 || lpg == 8 || lpg == 16)) {
+      // each group is a run of lpg lanes inside one 16-lane row: the two largest keys by DPP
+      float v1 = NEG, v2 = NEG;
 #pragma unroll
-      for (int i = 0; i < PL; ++i) {
-        const int e = i * 64 + lane;
-        if (e >= lo && e < hi && (key[i] > v1 || (key[i] == v1 && e < i1))) { v1 = key[i]; i1 = e; }
+      for (int j = 0; j < PL; ++j) {
+        const float k = key[j];
+        v2 = fmaxf(v2, fminf(v1, k));
+        v1 = fmaxf(v1, k);
       }
-      wave_argmax(v1, i1);
-      float v2 = NEG;
-      int i2 = 0x7fffffff;
+      top2_merge<0xb1>(v1, v2);                           // pairs
+      if (lpg >= 4) top2_merge<0x4e>(v1, v2);             // quads
+      if (lpg >= 8) top2_merge<0x141>(v1, v2);            // 8 lanes
+      if (lpg >= 16) top2_merge<0x140>(v1, v2);           // 16 lanes
+      if (lane % lpg == 0 && lane / lpg < ng) s_gscore[w][lane / lpg] = v1 + v2;
+      __builtin_amdgcn_wave_barrier();
+      if (lane < ng) gs = s_gscore[w][lane];
+    } else {
 #pragma unroll
-      for (int i = 0; i < PL; ++i) {
-        const int e = i * 64 + lane;
-        if (e >= lo && e < hi && e != i1 && (key[i] > v2 || (key[i] == v2 && e < i2))) { v2 = key[i]; i2 = e; }
+      for (int j = 0; j < PL; ++j) s_key[w][e0 + j] = key[j];
+      __builtin_amdgcn_wave_barrier();
+      if (lane < ng) {
+        float v1 = NEG, v2 = NEG;                         // two largest keys of the group
+#pragma unroll 8
+        for (int e = lane * gsz; e < (lane + 1) * gsz; ++e) {
+          const float k = s_key[w][e];
+          v2 = fmaxf(v2, fminf(v1, k));
+          v1 = fmaxf(v1, k);
+        }
+        gs = v1 + v2;
+        s_gscore[w][lane] = gs;
       }
-      wave_argmax(v2, i2);
-      if (lane == g) my_gscore = v1 + v2;
     }
-    uint64_t keep = 0;
-    for (int s = 0; s < p.topk_group; ++s) {
-      float v = ((keep >> lane) & 1ull) ? NEG : my_gscore;
-      int gi = (lane < p.n_group && !((keep >> lane) & 1ull)) ? lane : 0x7fffffff;
-      wave_argmax(v, gi);
-      keep |= 1ull << gi;
-    }
+    __builtin_amdgcn_wave_barrier();
+    int rank = 0;
+    if (lane < ng)
+#pragma unroll 8
+      for (int h = 0; h < ng; ++h) {
+        const float o = s_gscore[w][h];
+        rank += (o > gs || (o == gs && h < lane)) ? 1 : 0;
+      }
+    const uint64_t keep = __ballot(lane < ng && rank < p.topk_group);
 #pragma unroll
-    for (int i = 0; i < PL; ++i) {
-      const int e = i * 64 + lane;
-      elig[i] = elig[i] && e < E && ((keep >> (min(e / gsz, 63))) & 1ull);
-    }
+    for (int j = 0; j < PL; ++j)
+      if (e0 + j < E && !((keep >> ((e0 + j) / gsz)) & 1ull)) elig &= ~(1u << j);
   }
 
   // ---- top-k: k rounds of wave argmax over eligible, not yet chosen keys ----
+  uint64_t pk[PL];
+#pragma unroll
+  for (int j = 0; j < PL; ++j) pk[j] = pack_key(key[j], e0 + j);
   float selk[16];
   int seli[16];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    selk[j] = 0.f;
-    seli[j] = 0;
-    if (j < p.top_k) {
-      float v = NEG;
-      int idx = 0x7fffffff;
+  for (int r = 0; r < 16; ++r) {
+    selk[r] = 0.f;
+    seli[r] = 0;
+    if (r < p.top_k) {
+      uint64_t best = 0;                                  // below every packed key
 #pragma unroll
-      for (int i = 0; i < PL; ++i) {
-        const int e = i * 64 + lane;
-        if (elig[i] && (idx == 0x7fffffff || key[i] > v || (key[i] == v && e < idx))) { v = key[i]; idx = e; }
-      }
-      wave_argmax(v, idx);
-      selk[j] = v;
-      seli[j] = idx;
-#pragma unroll
-      for (int i = 0; i < PL; ++i)
-        if (i * 64 + lane == idx) elig[i] = false;
+      for (int j = 0; j < PL; ++j) best = umax64(best, ((elig >> j) & 1u) ? pk[j] : 0);
+      best = wave_max64(best);
+      // (the host guarantees at least top_k eligible experts, so best names one)
+      const int idx = min(max(packed_index(best), 0), E - 1);
+      seli[r] = idx;
+      selk[r] = packed_key(best);
+      const unsigned off = (unsigned)(idx - e0);
+      if (off < (unsigned)PL) elig &= ~(1u << off);
     }
   }
 
@@ -115,29 +251,33 @@ __global__ __launch_bounds__(256) void k_gate(GateProblem p) {
   if (p.gate == 0 && !p.renormalize) {
     float mm = NEG;
 #pragma unroll
-    for (int i = 0; i < PL; ++i) mm = fmaxf(mm, key[i]);
-    m = wave_max(mm);
+    for (int j = 0; j < PL; ++j) mm = fmaxf(mm, key[j]);
+    m = wave_max_fixed(mm);
     float part = 0.f;
 #pragma unroll
-    for (int i = 0; i < PL; ++i)
-      if (i * 64 + lane < E) part += expf(key[i] - m);
-    den = wave_sum(part);
+    for (int j = 0; j < PL; ++j)
+      if (e0 + j < E) part += expf(key[j] - m);
+    den = wave_sum_fixed(part);
   }
-  float w[16];
+  float wgt[16];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    w[j] = 0.f;
-    if (j < p.top_k) {
-      w[j] = (p.gate == 0) ? expf(selk[j] - m) : selk[j];
-      if (p.renormalize) den += w[j];
+  for (int r = 0; r < 16; ++r) {
+    wgt[r] = 0.f;
+    if (r < p.top_k) {
+      wgt[r] = (p.gate == 0) ? expf(selk[r] - m) : selk[r];
+      if (p.renormalize) den += wgt[r];
     }
   }
   const bool divide = p.renormalize || p.gate == 0;
+  // lane r < top_k writes slot r
   int oi = 0;
   float ow = 0.f;
 #pragma unroll
-  for (int j = 0; j < 16; ++j)
-    if (j == lane) { oi = seli[j]; ow = (divide ? w[j] / den : w[j]) * p.routed_scale; }
+  for (int r = 0; r < 16; ++r) {
+    oi = (lane == r) ? seli[r] : oi;
+    ow = (lane == r) ? wgt[r] : ow;
+  }
+  ow = (divide ? ow / den : ow) * p.routed_scale;
   if (lane < p.top_k) {
     p.topk_idx[t * p.top_k + lane] = oi;
     p.topk_w[t * p.top_k + lane] = ow;
@@ -146,14 +286,15 @@ __global__ __launch_bounds__(256) void k_gate(GateProblem p) {
 
 template <int PL>
 hipError_t launch_pl(const GateProblem& p, hipStream_t stream) {
-  const unsigned blocks = (unsigned)((p.T + 3) / 4);
-  hipLaunchKernelGGL(k_gate<PL>, dim3(blocks), dim3(256), 0, stream, p);
+  const unsigned blocks = (unsigned)((p.T + kWaves - 1) / kWaves);
+  hipLaunchKernelGGL(k_gate<PL>, dim3(blocks), dim3(64 * kWaves), 0, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gate(const GateProblem& p, hipStream_t stream) {
+  if (p.nsplit < 1) return hipErrorInvalidValue;
   const int pl = (p.E + 63) / 64;
   if (pl <= 1) return launch_pl<1>(p, stream);
   if (pl <= 2) return launch_pl<2>(p, stream);
