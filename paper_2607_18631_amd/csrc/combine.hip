@@ -3,69 +3,107 @@
 //   out[t] = bf16( sum_j topk_w[t,j] * y_perm[slot_row[t,j]]  (+ shared_y[t]) )
 //
 // float32 accumulation in slot order, the shared row last, one round-to-nearest-even.
-// The slot rows and gates are wave-uniform; each lane streams 16-byte vectors of the
-// k_local expert rows, so every row read is a fully coalesced 128-byte-per-8-lanes burst.
+// The token's local slots are compacted first (lane j holds slot j; a ballot gives each
+// local slot its position), so the row loop runs over local rows only, with no branch per
+// slot.  Each lane streams 16-byte vectors; per pass the shared row's loads are issued first
+// and the expert rows' loads two rows at a time, so several rows are in flight per wave.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace moe {
 namespace {
 
-__global__ __launch_bounds__(256) void k_combine(CombineProblem p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= p.T) return;
+constexpr int kWaves = 4;    // tokens per workgroup
+constexpr int U = 4;         // 16-byte vectors per lane and row in one pass
+
+__device__ __forceinline__ void fma_row(float (&acc)[U][8], const u32x4 (&y)[U], float w) {
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[u][2 * e] += w * bf16_to_f32(y[u][e] & 0xffffu);
+      acc[u][2 * e + 1] += w * bf16_to_f32(y[u][e] >> 16);
+    }
+}
+
+__global__ __launch_bounds__(64 * kWaves) void k_combine(CombineProblem p) {
+  __shared__ int s_row[kWaves][16];
+  __shared__ float s_w[kWaves][16];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * kWaves + wv;
+  if (t >= p.T) return;                                   // wave-uniform
   const int k = p.top_k;
+
+  // compact the local slots, keeping slot order
+  int r = -1;
+  float wj = 0.f;
+  if (lane < k) {
+    r = p.slot_row[t * k + lane];
+    if (r >= p.cap) r = -1;
+    wj = p.topk_w[t * k + lane];
+  }
+  const uint64_t act = __ballot(r >= 0);
+  const int nact = __popcll(act);
+  if (r >= 0) {
+    const int pos = __popcll(act & ((1ull << lane) - 1ull));
+    s_row[wv][pos] = r;
+    s_w[wv][pos] = wj;
+  }
+  __builtin_amdgcn_wave_barrier();
   int rows[16];
   float w[16];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    rows[j] = -1;
-    w[j] = 0.f;
-    if (j < k) {
-      rows[j] = p.slot_row[t * k + j];
-      if (rows[j] >= p.cap) rows[j] = -1;
-      w[j] = p.topk_w[t * k + j];
-    }
+  for (int a = 0; a < 16; ++a) {
+    rows[a] = a < nact ? __builtin_amdgcn_readfirstlane(s_row[wv][a]) : 0;
+    w[a] = a < nact ? __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s_w[wv][a]))) : 0.f;
   }
-  constexpr int U = 4;                       // 16-byte vectors per lane in flight per row
+
   const int nvec = p.d / 8;
+  const bf16_t* srow = p.shared_y ? p.shared_y + t * p.d : nullptr;
   for (int v0 = 0; v0 < nvec; v0 += 64 * U) {
+    u32x4 sy[U];
+    if (srow) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + u * 64 + lane;
+        sy[u] = v < nvec ? ld16(srow + v * 8) : u32x4{0, 0, 0, 0};
+      }
+    }
     float acc[U][8];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[u][e] = 0.f;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (rows[j] < 0) continue;
-      const bf16_t* yrow = p.y_perm + (int64_t)rows[j] * p.d;
-      u32x4 y[U];
+    for (int a = 0; a < 16; a += 2) {
+      if (a >= nact) break;
+      const bool two = a + 1 < nact;
+      const bf16_t* y0 = p.y_perm + (int64_t)rows[a] * p.d;
+      const bf16_t* y1 = p.y_perm + (int64_t)rows[two ? a + 1 : a] * p.d;
+      u32x4 ya[U], yb[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int v = v0 + u * 64 + lane;
-        y[u] = v < nvec ? ld16(yrow + v * 8) : u32x4{0, 0, 0, 0};
+        ya[u] = v < nvec ? ld16(y0 + v * 8) : u32x4{0, 0, 0, 0};
       }
+      if (two) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int v = v0 + u * 64 + lane;
+          yb[u] = v < nvec ? ld16(y1 + v * 8) : u32x4{0, 0, 0, 0};
+        }
+      }
+      fma_row(acc, ya, w[a]);
+      if (two) fma_row(acc, yb, w[a + 1]);
+    }
+    if (srow) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          acc[u][2 * e] += w[j] * bf16_to_f32(y[u][e] & 0xffffu);
-          acc[u][2 * e + 1] += w[j] * bf16_to_f32(y[u][e] >> 16);
+          acc[u][2 * e] += bf16_to_f32(sy[u][e] & 0xffffu);
+          acc[u][2 * e + 1] += bf16_to_f32(sy[u][e] >> 16);
         }
-    }
-    if (p.shared_y) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int v = v0 + u * 64 + lane;
-        if (v >= nvec) continue;
-        const u32x4 sy = ld16(p.shared_y + t * p.d + v * 8);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[u][2 * e] += bf16_to_f32(sy[e] & 0xffffu);
-          acc[u][2 * e + 1] += bf16_to_f32(sy[e] >> 16);
-        }
-      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -82,8 +120,8 @@ __global__ __launch_bounds__(256) void k_combine(CombineProblem p) {
 }  // namespace
 
 hipError_t launch_combine(const CombineProblem& p, hipStream_t stream) {
-  const unsigned blocks = (unsigned)((p.T + 3) / 4);
-  hipLaunchKernelGGL(k_combine, dim3(blocks), dim3(256), 0, stream, p);
+  const unsigned blocks = (unsigned)((p.T + kWaves - 1) / kWaves);
+  hipLaunchKernelGGL(k_combine, dim3(blocks), dim3(64 * kWaves), 0, stream, p);
   return hipGetLastError();
 }
 
