@@ -76,6 +76,31 @@ def gating_desc(sh):
     return g
 
 
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_swiglu_dsv3_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_18631_amd", "csrc", "gemm.hip")
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the SwiGLU GEMM from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary, or None when the kernel source changed since the counters were taken (or another
+    workload is benchmarked)."""
+    import hashlib
+    if workload != "dsv3" or not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    fields = {}
+    with open(TRAFFIC_SUMMARY) as f:
+        for line in f:
+            line = line.strip().strip("`")
+            if ":" in line and line.startswith(("traffic_bytes_per_launch", "kernel_source_sha256")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    with open(GEMM_SOURCE, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if fields.get("kernel_source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -108,6 +133,8 @@ def main():
     ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=8192, help="tokens of the oracle CPU baseline sample")
+    ap.add_argument("--copy-ref-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (reference dispatch for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs the MoE-layer forward of one expert-parallel rank on ONE GPU; "
@@ -126,6 +153,14 @@ def main():
     sh = inputs["shape"]
     layer = moe.DeviceLayer(inputs, device="cuda:0")
     torch.cuda.synchronize()
+    if args.copy_ref_mib > 0:
+        log(f"reference copy of {args.copy_ref_mib} MiB")
+        src = torch.ones(args.copy_ref_mib << 20, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     ev = HipEvents()
     nstep = len(moe.MOE_STEP_NAMES)
     log(f"warmup {args.warmup} steps")
@@ -196,7 +231,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic(args.workload),
             "launches_per_step": up_launches,
             "avg_launch_ms": float(up_ms / up_launches),
             "flops_per_step": up_flops,
