@@ -182,6 +182,34 @@ def main():
         ev.destroy(e)
     ms_step = wall * 1e3 / args.steps
 
+    # standalone permutation (histogram, scan, ranks and the row copy), the form whose bytes
+    # the HBM figure counts; inside the layer the row copy is folded into the up-projection
+    log("timing the standalone permutation")
+    T_, k_, cap_ = sh.T, sh.top_k, sh.capacity
+    p_idx = layer.region(moe.MOE_REGION_TOPK_IDX, torch.int32, (T_, k_))
+    p_counts = torch.empty(sh.E_local, dtype=torch.int32, device="cuda:0")
+    p_offsets = torch.empty(sh.E_local + 1, dtype=torch.int32, device="cuda:0")
+    p_row_token = torch.empty(cap_, dtype=torch.int32, device="cuda:0")
+    p_slot_row = torch.empty((T_, k_), dtype=torch.int32, device="cuda:0")
+    p_x_perm = torch.empty((cap_, sh.d), dtype=torch.bfloat16, device="cuda:0")
+    p_ws = moe.alloc_workspace(sh, moe.MOE_WS_PERMUTE, "cuda:0")
+
+    def permute_once():
+        moe.moe_permute(sh, p_idx, layer.x, p_counts, p_offsets, p_row_token, p_slot_row, p_x_perm, p_ws)
+
+    for _ in range(3):
+        permute_once()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record()
+    for _ in range(reps):
+        permute_once()
+    e1.record()
+    torch.cuda.synchronize()
+    permute_ms = e0.elapsed_time(e1) / reps
+    del p_x_perm
+
     # algorithmic work of this batch (from the routing the GPU produced)
     offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
     slot_row = layer.region(moe.MOE_REGION_SLOT_ROW, torch.int32, (sh.T, sh.top_k)).cpu().numpy()
@@ -220,7 +248,9 @@ def main():
                    "local_rows": n_loc, "parallelism": "one expert-parallel rank's share on 1 GPU"},
         "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
         "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-        "permute_gbs": perm_bytes / (avg[s["permute"]] * 1e-3) / 1e9,
+        "permute_gbs": perm_bytes / (permute_ms * 1e-3) / 1e9,
+        "permute_ms": permute_ms,
+        "permute_in_layer": "row copy folded into the up-projection (token rows read through row_token)",
         "combine_gbs": comb_bytes / (avg[s["combine"]] * 1e-3) / 1e9,
         "step_ms": {n: round(float(med[i]), 5) for n, i in s.items()},
         "gpu_event_ms_per_step": gpu_total / args.steps,

@@ -98,7 +98,8 @@ typedef enum moe_ws_region {
   MOE_REGION_OFFSETS = 3,    /* i32 [E_local+1]  */
   MOE_REGION_ROW_TOKEN = 4,  /* i32 [cap]        */
   MOE_REGION_SLOT_ROW = 5,   /* i32 [T, top_k]   */
-  MOE_REGION_X_PERM = 6,     /* bf16 [cap, d]    */
+  MOE_REGION_X_PERM = 6,     /* bf16 [cap, d]; written by moe_layer_forward only when T * d * 2 >= 2^32
+                                (otherwise the up-projection reads x through row_token) */
   MOE_REGION_Y_PERM = 7,     /* bf16 [cap, d]    */
   MOE_REGION_SHARED_Y = 8,   /* bf16 [T, d] (only when F_shared > 0) */
   MOE_REGION_COUNT_ = 9
@@ -183,6 +184,10 @@ int moe_combine(const moe_shape_t* shape, const void* y_perm, const int32_t* slo
                 const float* topk_w, const void* shared_y, void* out, void* stream);
 
 /* The whole layer: route -> permute -> grouped_ffn (+ shared expert) -> combine.
+ * The row copy of the permutation is folded into the up-projection (the paper's gathered
+ * first GEMM, Section 3.1): its token rows are read from x through row_token, so x_perm is
+ * not materialised (when T * d * 2 < 2^32; larger batches copy the rows first).  Results
+ * are identical either way.
  * ws13 / ws2 are required when F_shared > 0 and ignored otherwise.
  * ws: MOE_WS_LAYER bytes; its named regions hold the intermediates afterwards. */
 int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
@@ -194,7 +199,7 @@ typedef enum moe_step {
   MOE_STEP_ROUTER_GEMM = 0,   /* router logits (grouped GEMM, one group, f32 out)   */
   MOE_STEP_GATE = 1,          /* gating + top-k                                     */
   MOE_STEP_HISTOGRAM = 2,     /* per-chunk histogram + scan over chunks             */
-  MOE_STEP_PERMUTE = 3,       /* offsets, stable ranks, row copy                    */
+  MOE_STEP_PERMUTE = 3,       /* offsets, stable ranks (+ row copy when not folded) */
   MOE_STEP_FFN_UP = 4,        /* routed experts: W1/W3 GEMM + SwiGLU                */
   MOE_STEP_FFN_DOWN = 5,      /* routed experts: W2 GEMM                            */
   MOE_STEP_SHARED_UP = 6,     /* shared expert: W1/W3 GEMM + SwiGLU (if F_shared)   */

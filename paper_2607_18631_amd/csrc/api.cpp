@@ -241,11 +241,20 @@ struct SharedOperands {
   int64_t T = 0;
 };
 
+// Gathered rows for the up-projection: row r of the grouped part is token row_index[r] of X
+// (X has x_rows rows); row_index == nullptr means X is already in expert order.
+struct Gather {
+  const int32_t* row_index = nullptr;
+  int64_t x_rows = 0;
+};
+
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
            int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0,
-           const SharedOperands* sh = nullptr) {
+           const SharedOperands* sh = nullptr, Gather gather = Gather{}) {
   moe::GemmProblem up{};
   up.X = static_cast<const moe::bf16_t*>(X);
+  up.row_index = gather.row_index;
+  up.x_rows = gather.x_rows;
   up.ldx = d;
   up.offsets = offsets;
   up.groups = groups;
@@ -267,6 +276,8 @@ int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, cons
   CHECK(hip_status(moe::launch_grouped_gemm(up, st), "expert up-projection launch"));
   if (mark) CHECK(mark(down_step));
   moe::GemmProblem dn = up;
+  dn.row_index = nullptr;
+  dn.x_rows = 0;
   dn.X = static_cast<const moe::bf16_t*>(act);
   dn.ldx = F;
   dn.W = static_cast<const moe::bf16_t*>(w2);
@@ -442,9 +453,12 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
 
   if (mark) CHECK(mark(MOE_STEP_ROUTER_GEMM));
   CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, nullptr, at<float>(ws, L.logits), st, mark));
+  // the permutation folded into the up-projection's copies: its token rows are read from x
+  // through row_token (no x_perm round trip), where per-lane 32-bit offsets reach all of x
+  const bool fused_gather = shape->T * (int64_t)shape->d * 2 < (int64_t(1) << 32);
   if (mark) CHECK(mark(MOE_STEP_HISTOGRAM));
-  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, at<void>(ws, L.perm_ws), st,
-                   mark));
+  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, fused_gather ? nullptr : x_perm,
+                   at<void>(ws, L.perm_ws), st, mark));
   // a shared expert as wide as the routed ones runs inside the routed launches (its tiles
   // interleaved with the experts'), otherwise in launches of its own
   const bool merged = shape->F_shared > 0 && shape->F_shared == shape->F;
@@ -458,8 +472,13 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     so.T = shape->T;
   }
   if (mark) CHECK(mark(MOE_STEP_FFN_UP));
-  CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, at<void>(ws, L.act),
-               y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr));
+  Gather gather;
+  if (fused_gather) {
+    gather.row_index = row_token;
+    gather.x_rows = shape->T;
+  }
+  CHECK(do_ffn(fused_gather ? x : x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F,
+               at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr, gather));
   if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
   if (shape->F_shared > 0 && !merged)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,

@@ -196,6 +196,7 @@ __device__ __forceinline__ int first_tile_slot() {
 struct TileDesc {
   int row0, row_end, ni;
   int kb, ke, kc;            // K slices [kb, ke) of K chunk kc
+  const int32_t* rows;       // gathered rows: tile row r is X row rows[row0 + r] (else row0 + r)
   const bf16_t* X;
   const bf16_t* W;
   void* Y;
@@ -218,6 +219,7 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
     d.W = p.W2;
     d.X = p.X2;
     d.Y = p.Y2;
+    d.rows = nullptr;
   } else {
     const int t = tile - x_before;                        // index among the grouped tiles
     int lo = 0, hi = ts.groups;                           // s_tp[groups] == grouped tiles > t
@@ -232,6 +234,7 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
     d.W = p.W + (int64_t)g * p.w_group_stride;
     d.X = p.X;
     d.Y = p.Y;
+    d.rows = p.row_index;
   }
   const int mt = (d.row_end - row0g + BM - 1) / BM;
   // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
@@ -269,13 +272,26 @@ struct CopyPlan {
   __device__ __forceinline__ void setup(const GemmProblem& p, const TileDesc& t, int wave, int lane) {
     const int li_row = lane / Z::CPR, li_pc = lane % Z::CPR;
     const int K = p.K;
-    xbase = reinterpret_cast<const char*>(t.X + (int64_t)t.row0 * p.ldx);
     const int last = t.row_end - 1 - t.row0;
+    if (t.rows) {
+      // gathered rows: the lane's own source row (the launcher keeps x_rows * ldx * 2 < 2^32)
+      xbase = reinterpret_cast<const char*>(t.X);
+      const int top = (int)p.x_rows - 1;
 #pragma unroll
-    for (int j = 0; j < LX; ++j) {
-      const int r = (wave + NW * j) * RPI + li_row;         // tile row
-      xchunk[j] = li_pc ^ Z::f(r);
-      xoff[j] = (uint32_t)(min(r, last) * p.ldx * 2 + xchunk[j] * 16);
+      for (int j = 0; j < LX; ++j) {
+        const int r = (wave + NW * j) * RPI + li_row;
+        xchunk[j] = li_pc ^ Z::f(r);
+        const int src = min(max(t.rows[t.row0 + min(r, last)], 0), top);
+        xoff[j] = (uint32_t)((int64_t)src * p.ldx * 2 + xchunk[j] * 16);
+      }
+    } else {
+      xbase = reinterpret_cast<const char*>(t.X + (int64_t)t.row0 * p.ldx);
+#pragma unroll
+      for (int j = 0; j < LX; ++j) {
+        const int r = (wave + NW * j) * RPI + li_row;         // tile row
+        xchunk[j] = li_pc ^ Z::f(r);
+        xoff[j] = (uint32_t)(min(r, last) * p.ldx * 2 + xchunk[j] * 16);
+      }
     }
 #pragma unroll
     for (int j = 0; j < LW; ++j) {
@@ -740,6 +756,8 @@ int logits_splits(int64_t T, int E, int K) {
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   if (p.ksplit > 1 && (p.epi != EPI_F32 || p.offsets != nullptr || p.rows2 > 0)) return hipErrorInvalidValue;
+  // gathered rows: the per-lane 32-bit source offsets must reach every row of X
+  if (p.row_index && (p.x_rows < 1 || p.x_rows * p.ldx * 2 >= (int64_t(1) << 32))) return hipErrorInvalidValue;
   // 256 x 256 tiles, 8 waves, two 64-wide K slices in flight: the best measured on the DeepSeek-V3,
   // Mixtral and skewed workloads (largest reuse per byte copied into LDS)
   int cfg_swiglu = 6, cfg_bf16 = 6;

@@ -39,6 +39,10 @@ struct GemmProblem {
   // chunks, chunk c writing its fp32 partial product at Y + c * y_split_stride
   int32_t ksplit;
   int64_t y_split_stride;
+  // gathered rows (the permutation folded into the copies): when row_index is set, row r of
+  // the grouped part is row row_index[r] of X (X has x_rows rows; indices are clamped to them)
+  const int32_t* row_index;
+  int64_t x_rows;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
@@ -71,7 +75,7 @@ struct PermuteProblem {
   int32_t* offsets;           // [E_local + 1]
   int32_t* row_token;         // [cap]
   int32_t* slot_row;          // [T, top_k]
-  bf16_t* x_perm;             // [cap, d]
+  bf16_t* x_perm;             // [cap, d]; nullptr: no row copy (the GEMM gathers the rows itself)
   int64_t cap;                // rows of row_token / x_perm
   int32_t* blk_count;         // workspace [nblk, E_local]
   int32_t* blk_base;          // workspace [nblk, E_local]

@@ -10,7 +10,8 @@
 //                      row = offsets[e] + chunk_base[c][e] + rank,
 //                  then row_token / slot_row
 //   k_gather       per token: the bit-exact copy of the token row to each of its local
-//                  rows (read once, written k_local times, 16-byte vectors)
+//                  rows (read once, written k_local times, 16-byte vectors); skipped when
+//                  the caller's GEMM reads the token rows through row_token itself
 //
 // The in-chunk rank uses wavefront ballots instead of atomics, so the order inside an
 // expert is ascending token (a stable counting sort) and run-to-run identical: for every
@@ -229,6 +230,7 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*bet
   hipLaunchKernelGGL(k_rank, dim3((unsigned)nblk), dim3(64 * RW), (p.E_local + 1) * sizeof(int), stream, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (p.x_perm == nullptr) return hipSuccess;
   hipLaunchKernelGGL(k_gather, dim3((unsigned)((p.T + 3) / 4)), dim3(256), 0, stream, p);
   return hipGetLastError();
 }

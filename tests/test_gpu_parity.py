@@ -58,6 +58,27 @@ def _intermediates(layer):
     }
 
 
+def _check_standalone_permute(layer, inputs, inter, n):
+    """moe_permute on the layer's routing: same indices as the layer, x_perm rows bit-exact copies
+    (the layer itself reads the token rows through row_token and writes no x_perm)."""
+    sh = layer.shape
+    dev = "cuda"
+    T, k, cap = sh.T, sh.top_k, sh.capacity
+    idx = layer.region(moe.MOE_REGION_TOPK_IDX, torch.int32, (T, k))
+    counts = torch.empty(sh.E_local, dtype=torch.int32, device=dev)
+    offsets = torch.empty(sh.E_local + 1, dtype=torch.int32, device=dev)
+    row_token = torch.empty(cap, dtype=torch.int32, device=dev)
+    slot_row = torch.empty((T, k), dtype=torch.int32, device=dev)
+    x_perm = torch.empty((cap, sh.d), dtype=torch.bfloat16, device=dev)
+    moe.moe_permute(sh, idx, layer.x, counts, offsets, row_token, slot_row, x_perm,
+                    moe.alloc_workspace(sh, moe.MOE_WS_PERMUTE))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(offsets.cpu().numpy(), inter["offsets"])
+    np.testing.assert_array_equal(row_token.cpu().numpy()[:n], inter["row_token"][:n])
+    np.testing.assert_array_equal(slot_row.cpu().numpy(), inter["slot_row"])
+    np.testing.assert_array_equal(dev_bits(x_perm[:n]), inputs["x"][inter["row_token"][:n]])
+
+
 def _check_permutation(sh, inter, g_idx):
     counts, offsets = oracle.counts_offsets(g_idx, sh.e_begin, sh.E_local)
     row_token, slot_row = oracle.permutation(g_idx, sh.e_begin, sh.E_local)
@@ -83,9 +104,8 @@ def test_small_layer_parity(name):
     inter = _intermediates(layer)
     np.testing.assert_array_equal(inter["topk_w"], g_w)
     n = _check_permutation(sh, inter, g_idx)
-    # x_perm rows are bit-exact copies
-    x_perm = dev_bits(layer.region(moe.MOE_REGION_X_PERM, torch.bfloat16, (sh.capacity, sh.d)))
-    np.testing.assert_array_equal(x_perm[:n], inputs["x"][inter["row_token"][:n]])
+    # the standalone permutation: same indices, x_perm rows bit-exact copies
+    _check_standalone_permute(layer, inputs, inter, n)
     # per-expert MLP rows
     y_perm = oracle.bf16_to_f64(dev_bits(layer.region(moe.MOE_REGION_Y_PERM, torch.bfloat16,
                                                        (sh.capacity, sh.d))))
@@ -219,8 +239,7 @@ def test_full_workload_parity(name):
     inter = _intermediates(layer)
     np.testing.assert_array_equal(inter["topk_w"], g_w)
     n = _check_permutation(sh, inter, g_idx)
-    x_perm = dev_bits(layer.region(moe.MOE_REGION_X_PERM, torch.bfloat16, (sh.capacity, sh.d))[:n])
-    np.testing.assert_array_equal(x_perm, inputs["x"][inter["row_token"][:n]])
+    _check_standalone_permute(layer, inputs, inter, n)
     # sampled output rows (plus every near-tie token)
     rng = np.random.default_rng(123)
     toks = np.unique(np.concatenate([rng.choice(sh.T, size=min(sh.T, 48), replace=False), np.array(near, int)]))
