@@ -229,6 +229,11 @@ def main():
     gemm_ms = sum(avg[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
     perm_bytes = (tok_local + n_loc) * d * 2 + T * k * 8 + n_loc * 4
     comb_bytes = n_loc * d * 2 + (T * d * 2 if Fs > 0 else 0) + T * d * 2 + T * k * 8
+    # whole-layer algorithmic HBM bytes (the decode-step figure): weights of the experts that
+    # received rows, shared-expert and router weights, token rows in and out, routing arrays
+    active = int((np.diff(offsets) > 0).sum())
+    layer_bytes = (active * 3 * d * F * 2 + 3 * d * Fs * 2 + sh.E * d * 2 + 2 * T * d * 2
+                   + T * k * 8)
     achieved = up_flops / (up_ms * 1e-3) / 1e12
     res = {
         "metric": "MoE-layer tokens/s + grouped-GEMM TFLOP/s (% bf16 MFMA peak), 1 MI355X",
@@ -252,6 +257,8 @@ def main():
         "permute_ms": permute_ms,
         "permute_in_layer": "row copy folded into the up-projection (token rows read through row_token)",
         "combine_gbs": comb_bytes / (avg[s["combine"]] * 1e-3) / 1e9,
+        "layer_hbm_gbs": layer_bytes / (ms_step * 1e-3) / 1e9,
+        "active_local_experts": active,
         "step_ms": {n: round(float(med[i]), 5) for n, i in s.items()},
         "gpu_event_ms_per_step": gpu_total / args.steps,
         "roofline": {
