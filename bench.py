@@ -101,6 +101,63 @@ def measured_traffic(workload):
     return float(fields["traffic_bytes_per_launch"])
 
 
+def timed_median(fn, reps, rounds=3, warmup=10):
+    """Median over `rounds` of the median per-call time (ms) of `reps` calls, each call between
+    two events on the current stream, after `warmup` calls."""
+    import numpy as np
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    meds = []
+    for _ in range(rounds):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record()
+        for i in range(reps):
+            fn()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        meds.append(float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])))
+    return float(np.median(meds))
+
+
+def crossover_run():
+    """The paper's RQ4 kernel-crossover workload: per-token latency over the global token count
+    me * E / top_k, for the grouped expert MLP alone (exactly me rows per local expert, the
+    figure's single-card expert compute) and for the whole layer on that many tokens.  Protocol:
+    warmup 10, 200 calls per round for me < 16 else 50, median of 3 round medians."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    rows = []
+    for me in wl.CROSSOVER_ME:
+        w = wl.crossover(me)
+        inputs = wl.make_inputs(w)
+        sh = inputs["shape"]
+        layer = moe.DeviceLayer(inputs, device="cuda:0")
+        reps = 200 if me < 16 else 50
+        n = me * sh.E_local
+        offsets = torch.arange(0, n + 1, me, dtype=torch.int32, device="cuda:0")
+        x_perm = layer.x[:n].contiguous()                  # n = T / 4 distinct token rows
+        ffn_sh = sh.replace(T=n, top_k=1)              # capacity n rows
+        y = torch.empty((n, sh.d), dtype=torch.bfloat16, device="cuda:0")
+        ws = moe.alloc_workspace(ffn_sh, moe.MOE_WS_FFN, "cuda:0")
+        t_ffn = timed_median(lambda: moe.moe_grouped_ffn(ffn_sh, x_perm, offsets, layer.w13, layer.w2, y, ws), reps)
+        t_layer = timed_median(layer.forward, reps)
+        tokens = me * sh.E // sh.top_k
+        rows.append({"me": me, "global_tokens": tokens, "expert_mlp_us": t_ffn * 1e3,
+                     "expert_mlp_us_per_token": t_ffn * 1e3 / tokens,
+                     "expert_mlp_tflops": 6.0 * sh.d * sh.F * n / (t_ffn * 1e-3) / 1e12,
+                     "layer_us": t_layer * 1e3, "layer_us_per_token": t_layer * 1e3 / tokens})
+        log(f"me={me}: expert MLP {t_ffn * 1e3:.1f} us ({rows[-1]['expert_mlp_us_per_token']:.4f} us/token), "
+            f"layer {t_layer * 1e3:.1f} us")
+        del layer, x_perm, y, ws
+        torch.cuda.empty_cache()
+    return rows
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -133,6 +190,9 @@ def main():
     ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=8192, help="tokens of the oracle CPU baseline sample")
+    ap.add_argument("--crossover", action="store_true",
+                    help="the paper's RQ4 kernel-crossover sweep (E=64, d=2048, F=1408, top-2, 8 local experts, "
+                         "me = tokens per expert) instead of the layer benchmark")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (reference dispatch for HBM counters)")
     args = ap.parse_args()
@@ -148,6 +208,16 @@ def main():
     from paper_2607_18631_amd import workloads as wl
 
     torch.cuda.set_device(0)
+    if args.crossover:
+        rows = crossover_run()
+        print(json.dumps({"metric": "per-token latency, kernel-crossover shape (E=64, d=2048, F=1408, top-2, "
+                                    "8 local experts), 1 MI355X",
+                          "unit": "us/token", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "protocol": "warmup 10; 200 calls per round for me < 16 else 50; median of 3 round "
+                                      "medians; HIP events on the library's stream",
+                          "rows": rows}), flush=True)
+        return
     log(f"generating inputs of workload {args.workload}")
     inputs = wl.make_inputs(args.workload)
     sh = inputs["shape"]

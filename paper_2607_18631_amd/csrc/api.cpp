@@ -3,6 +3,7 @@
 // returns its status without any HIP call; a valid call only enqueues work on `stream`.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -250,8 +251,9 @@ struct Gather {
 
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
            int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0,
-           const SharedOperands* sh = nullptr, Gather gather = Gather{}) {
+           const SharedOperands* sh = nullptr, Gather gather = Gather{}, int64_t rows_hint = 0) {
   moe::GemmProblem up{};
+  up.rows_hint = rows_hint > 0 ? rows_hint : (groups > 0 ? (rows + groups - 1) / groups : rows);
   up.X = static_cast<const moe::bf16_t*>(X);
   up.row_index = gather.row_index;
   up.x_rows = gather.x_rows;
@@ -477,8 +479,11 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     gather.row_index = row_token;
     gather.x_rows = shape->T;
   }
+  // expected rows per local expert (uniform routing): T * top_k / E
+  const int64_t rows_hint = std::max<int64_t>(1, shape->T * shape->top_k / shape->E);
   CHECK(do_ffn(fused_gather ? x : x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F,
-               at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr, gather));
+               at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr, gather,
+               rows_hint));
   if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
   if (shape->F_shared > 0 && !merged)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,

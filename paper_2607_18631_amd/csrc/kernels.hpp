@@ -43,6 +43,9 @@ struct GemmProblem {
   // the grouped part is row row_index[r] of X (X has x_rows rows; indices are clamped to them)
   const int32_t* row_index;
   int64_t x_rows;
+  // expected rows per group (0 = unknown): selects the tile shape (the row counts themselves
+  // stay on the device)
+  int64_t rows_hint;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);

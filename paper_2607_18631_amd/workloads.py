@@ -18,6 +18,12 @@ appendix's kernel-crossover protocol).  The five workloads are:
   k2decode  T=64    d=7168 E=384 top-8 sigmoid, 48 local experts of F=2048 plus
             one shared expert of width 2048 (one decode step of one EP8 rank)
 
+The kernel-crossover workload of the paper's RQ4 figure (``crossover(me)``): E=64
+experts of width F=1408 on hidden size d=2048, top-2 softmax gating (renormalised), one
+rank holding 8 local experts (world size 8); ``me`` is the expert multiplicity (tokens per
+expert), the batch has me * E / top_k tokens, and per-token latency is quoted over that
+global token count.  ``CROSSOVER_ME`` lists the multiplicities the figure reports.
+
 Input recipe (all seeded, synthetic):
   * every tensor is drawn as float32 N(0, std) from its own numpy PCG64 stream
     ``SeedSequence(seed, spawn_key=(tensor_id, index))`` and rounded to bf16 with
@@ -99,6 +105,17 @@ WORKLOADS = {
                                               F_shared=2048, gate=GATE_SIGMOID),
                          router_std=7168 ** -0.5),
 }
+
+
+# kernel-crossover workload (the paper's RQ4 figure; me = 512 is absent from its data)
+CROSSOVER_ME = (2, 4, 8, 16, 32, 64, 128, 256, 1024)
+
+
+def crossover(me: int) -> Workload:
+    """The kernel-crossover shape at expert multiplicity ``me`` (me * 64 / 2 global tokens)."""
+    E, top_k = 64, 2
+    return Workload(f"crossover_me{me}", MoEShape(T=me * E // top_k, d=2048, E=E, top_k=top_k, F=1408,
+                                                  E_local=8), router_std=2048 ** -0.5)
 
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
