@@ -763,12 +763,13 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   // gathered rows: the per-lane 32-bit source offsets must reach every row of X
   if (p.row_index && (p.x_rows < 1 || p.x_rows * p.ldx * 2 >= (int64_t(1) << 32))) return hipErrorInvalidValue;
   // 256 x 256 tiles, 8 waves, two 64-wide K slices in flight: the best measured on the DeepSeek-V3,
-  // Mixtral and skewed workloads (largest reuse per byte copied into LDS).  With at most 128
-  // expected rows per group (decode steps, small expert multiplicity) the launch is a weight
-  // stream over few m-tiles: 64 x 128 tiles spread it over 4x more workgroups (measured
-  // 1.4-1.8x faster at 2-128 rows per expert, slower from ~1000).
-  const bool few_rows = p.rows_hint > 0 && p.rows_hint <= 128 && p.rows2 <= 512;
-  int cfg_swiglu = few_rows ? 20 : 6, cfg_bf16 = few_rows ? 20 : 6;
+  // Mixtral and skewed workloads (largest reuse per byte copied into LDS; also whenever a large
+  // dense extra group shares the launch).  With few expected rows per group the launch is a
+  // weight stream over few m-tiles, spread over more workgroups by smaller tiles: 64 x 128 up to
+  // 128 rows per group (1.4-1.8x faster at 2-128 rows), 128 x 256 up to 512 (1.1-1.5x).
+  const bool small_extra = p.rows2 <= 512;
+  const int tier = (p.rows_hint > 0 && small_extra) ? (p.rows_hint <= 128 ? 20 : p.rows_hint <= 512 ? 5 : 6) : 6;
+  int cfg_swiglu = tier, cfg_bf16 = tier;
 #ifdef MOE_GEMM_SWEEP
   if (g_force_cfg[EPI_SWIGLU] >= 0) cfg_swiglu = g_force_cfg[EPI_SWIGLU];
   if (g_force_cfg[EPI_BF16] >= 0) cfg_bf16 = g_force_cfg[EPI_BF16];
