@@ -23,7 +23,11 @@ What it computes (one MoE layer on one expert-parallel rank):
                           monotone [E_local + 1] row-offset array of the paper's
                           kernel-generation section (expert e owns rows
                           [offs[e], offs[e + 1]))
-  8. permutation          rows grouped by expert, ascending token inside an expert
+  8. permutation          rows grouped by expert, ascending token inside an expert;
+                          masked-decode layout (expert_capacity C > 0, the equal-stride
+                          capacity segments of the kernel-generation section): expert e
+                          owns rows [e C, e C + min(count_e, C)); a slot whose rank
+                          inside its expert (ascending token) is >= C is dropped
   9. expert FFN (SwiGLU)  y = W2_e (silu(W1_e x) * (W3_e x)); the forward composes
                           the two GEMMs of the expert MLP (Section 4, kernel
                           generation / engine registration)
@@ -154,28 +158,68 @@ def local_expert(topk_idx: np.ndarray, e_begin: int, E_local: int) -> np.ndarray
     return np.where((le >= 0) & (le < E_local), le, -1)
 
 
-def counts_offsets(topk_idx: np.ndarray, e_begin: int, E_local: int):
-    """counts[e] = local slots routed to local expert e; offsets = [0, cumsum(counts)]."""
+def counts_offsets(topk_idx: np.ndarray, e_begin: int, E_local: int, expert_capacity: int = 0):
+    """counts[e] = local slots routed to local expert e (before any capacity drop);
+    offsets = [0, cumsum(counts)], or the equal-stride segment starts e * C (e = 0 .. E_local)
+    in the masked-decode layout."""
     le = local_expert(topk_idx, e_begin, E_local)
     counts = np.bincount(le[le >= 0], minlength=E_local).astype(np.int32)
-    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    if expert_capacity > 0:
+        offsets = (np.arange(E_local + 1) * expert_capacity).astype(np.int32)
+    else:
+        offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     return counts, offsets
 
 
-def permutation(topk_idx: np.ndarray, e_begin: int, E_local: int):
+def expert_rank(topk_idx: np.ndarray, e_begin: int, E_local: int) -> np.ndarray:
+    """Rank of every local slot among the slots of its expert in ascending token order
+    (the token-major slot list; two slots of one token never share an expert), -1 elsewhere."""
+    T, k = topk_idx.shape
+    le = local_expert(topk_idx, e_begin, E_local).reshape(-1)
+    slots = np.nonzero(le >= 0)[0]
+    order = slots[np.argsort(le[slots], kind="stable")]              # stable: token order kept
+    counts = np.bincount(le[slots], minlength=E_local)
+    first = np.concatenate([[0], np.cumsum(counts)])[:-1]
+    rank = np.full(T * k, -1, np.int64)
+    rank[order] = np.arange(order.size) - first[le[order]]
+    return rank.reshape(T, k)
+
+
+def keep_mask(topk_idx: np.ndarray, e_begin: int, E_local: int, expert_capacity: int = 0) -> np.ndarray:
+    """Slots that reach this rank's experts: local, and (masked-decode layout) ranked below the
+    expert capacity inside their expert."""
+    rank = expert_rank(topk_idx, e_begin, E_local)
+    keep = rank >= 0
+    if expert_capacity > 0:
+        keep &= rank < expert_capacity
+    return keep
+
+
+def permutation(topk_idx: np.ndarray, e_begin: int, E_local: int, expert_capacity: int = 0):
     """Expert-contiguous row order: row_token[r] = token of row r; slot_row[t, j] = row or -1.
 
     Rows of one expert are in ascending token order (a stable counting sort of the
-    token-major slot list).
+    token-major slot list).  Masked-decode layout (expert_capacity C > 0): row_token has
+    E_local * C entries (-1 for rows past an expert's valid prefix); slot (t, j) of local
+    expert e with rank r < C sits in row e * C + r, a slot with r >= C is dropped (-1).
     """
     T, k = topk_idx.shape
-    le = local_expert(topk_idx, e_begin, E_local).reshape(-1)       # token-major slot list
-    slots = np.nonzero(le >= 0)[0]
-    order = slots[np.argsort(le[slots], kind="stable")]              # stable: token order kept
-    row_token = (order // k).astype(np.int32)
-    slot_row = np.full(T * k, -1, np.int32)
-    slot_row[order] = np.arange(order.size, dtype=np.int32)
-    return row_token, slot_row.reshape(T, k)
+    le = local_expert(topk_idx, e_begin, E_local)
+    rank = expert_rank(topk_idx, e_begin, E_local)
+    if expert_capacity > 0:
+        keep = (rank >= 0) & (rank < expert_capacity)
+        slot_row = np.where(keep, le * expert_capacity + rank, -1).astype(np.int32)
+        row_token = np.full(E_local * expert_capacity, -1, np.int32)
+        tt, jj = np.nonzero(keep)
+        row_token[slot_row[tt, jj]] = tt
+        return row_token, slot_row
+    counts = np.bincount(le[le >= 0], minlength=E_local)
+    first = np.concatenate([[0], np.cumsum(counts)])
+    slot_row = np.where(rank >= 0, first[np.maximum(le, 0)] + rank, -1).astype(np.int32)
+    row_token = np.zeros(int(counts.sum()), np.int32)
+    tt, jj = np.nonzero(rank >= 0)
+    row_token[slot_row[tt, jj]] = tt
+    return row_token, slot_row
 
 
 # ----------------------------------------------------------------------------------------
@@ -210,15 +254,19 @@ def combine(y_rows: np.ndarray, slot_row: np.ndarray, topk_w: np.ndarray, shared
 
 
 def expert_outputs_for_tokens(xd: np.ndarray, topk_idx: np.ndarray, topk_w: np.ndarray, shape,
-                              w13_bits, w2_bits, ws13_bits=None, ws2_bits=None) -> np.ndarray:
+                              w13_bits, w2_bits, ws13_bits=None, ws2_bits=None, keep=None) -> np.ndarray:
     """Layer output rows for a set of tokens, straight from the definition.
 
     xd: [n, d] float64 token rows; topk_idx / topk_w: their routing.  Each local
     expert's weights are decoded once and applied to the tokens that chose it.
+    keep: optional [n, k] mask of the slots that reach the experts (the masked-decode
+    layout drops slots past an expert's capacity; the mask comes from the whole batch).
     """
     n = xd.shape[0]
     out = np.zeros((n, shape.d), np.float64)
     le = local_expert(topk_idx, shape.e_begin, shape.E_local)
+    if keep is not None:
+        le = np.where(keep, le, -1)
     for e in np.unique(le[le >= 0]):
         rows, slots = np.nonzero(le == e)
         y = swiglu_ffn(xd[rows], bf16_to_f64(w13_bits[e]), bf16_to_f64(w2_bits[e]))
@@ -241,9 +289,11 @@ def layer_forward(inputs: dict, routing=None):
     idx, w, keys = route(xd, bf16_to_f64(inputs["w_router"]), sh, inputs.get("bias"))
     if routing is not None:
         idx, w = routing
-    counts, offsets = counts_offsets(idx, sh.e_begin, sh.E_local)
-    row_token, slot_row = permutation(idx, sh.e_begin, sh.E_local)
+    C = getattr(sh, "expert_capacity", 0)
+    counts, offsets = counts_offsets(idx, sh.e_begin, sh.E_local, C)
+    row_token, slot_row = permutation(idx, sh.e_begin, sh.E_local, C)
+    keep = keep_mask(idx, sh.e_begin, sh.E_local, C) if C > 0 else None
     out = expert_outputs_for_tokens(xd, idx, w, sh, inputs["w13"], inputs["w2"],
-                                    inputs.get("ws13"), inputs.get("ws2"))
+                                    inputs.get("ws13"), inputs.get("ws2"), keep)
     return {"topk_idx": idx, "topk_w": w, "keys": keys, "counts": counts, "offsets": offsets,
             "row_token": row_token, "slot_row": slot_row, "out": out}

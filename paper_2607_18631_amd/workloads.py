@@ -70,13 +70,16 @@ class MoEShape:
     topk_group: int = 1    # groups kept per token when n_group > 1
     renormalize: int = 1   # renormalise gates over the chosen experts
     routed_scale: float = 1.0
+    expert_capacity: int = 0   # > 0: masked-decode layout, rows [e C, e C + C) per local expert
 
     def replace(self, **kw) -> "MoEShape":
         return dataclasses.replace(self, **kw)
 
     @property
     def capacity(self) -> int:
-        """Upper bound of local (token, expert) rows: T * min(top_k, E_local)."""
+        """Rows of the permuted buffers: T * min(top_k, E_local), or E_local * expert_capacity."""
+        if self.expert_capacity > 0:
+            return self.E_local * self.expert_capacity
         return self.T * min(self.top_k, self.E_local)
 
 

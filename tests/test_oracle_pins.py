@@ -235,6 +235,84 @@ def test_counts_offsets_permutation_bruteforce(E, k, e_begin, E_local, T):
                 assert row_token[r] == t and offsets[idx[t, j] - e_begin] <= r < offsets[idx[t, j] - e_begin + 1]
 
 
+def _brute_capacity_perm(idx, e_begin, E_local, C):
+    """The masked-decode drop rule by a sequential walk: tokens in order, slots in order, each
+    local expert keeps its first C slots in rows e*C, e*C+1, ...; the rest are dropped."""
+    T, k = idx.shape
+    taken = [0] * E_local
+    slot_row = [[-1] * k for _ in range(T)]
+    row_token = [-1] * (E_local * C)
+    for t in range(T):
+        for j in range(k):
+            e = int(idx[t, j]) - e_begin
+            if 0 <= e < E_local:
+                if taken[e] < C:
+                    slot_row[t][j] = e * C + taken[e]
+                    row_token[e * C + taken[e]] = t
+                taken[e] += 1
+    return taken, row_token, slot_row
+
+
+def test_capacity_layout_hand():
+    """Experts 0..2 local, capacity 2: expert 0 keeps tokens 0, 1 and drops 2, 3; expert 1 keeps
+    tokens 0, 2 and drops 3; expert 2 keeps token 1."""
+    idx = np.array([[0, 1], [0, 2], [1, 0], [0, 1]], np.int32)
+    counts, offsets = oracle.counts_offsets(idx, 0, 3, 2)
+    row_token, slot_row = oracle.permutation(idx, 0, 3, 2)
+    assert counts.tolist() == [4, 3, 1] and offsets.tolist() == [0, 2, 4, 6]
+    assert slot_row.tolist() == [[0, 2], [1, 4], [3, -1], [-1, -1]]
+    assert row_token.tolist() == [0, 1, 0, 2, 1, -1]
+    assert oracle.keep_mask(idx, 0, 3, 2).tolist() == [[True, True], [True, True], [True, False], [False, False]]
+
+
+@pytest.mark.parametrize("E,k,e_begin,E_local,T,C", [(8, 2, 0, 8, 40, 1), (8, 2, 0, 8, 40, 6), (16, 4, 4, 5, 33, 3),
+                                                     (32, 8, 0, 32, 17, 2), (12, 3, 11, 1, 25, 4),
+                                                     (8, 3, 2, 4, 29, 100)])
+def test_capacity_layout_bruteforce(E, k, e_begin, E_local, T, C):
+    rng = np.random.default_rng(E * 1000 + k * 10 + C)
+    idx = np.array([rng.permutation(E)[:k] for _ in range(T)], np.int32)
+    counts, offsets = oracle.counts_offsets(idx, e_begin, E_local, C)
+    row_token, slot_row = oracle.permutation(idx, e_begin, E_local, C)
+    taken, brt, bsr = _brute_capacity_perm(idx, e_begin, E_local, C)
+    assert counts.tolist() == taken
+    assert offsets.tolist() == [e * C for e in range(E_local + 1)]
+    assert row_token.tolist() == brt and slot_row.tolist() == bsr
+    assert (oracle.keep_mask(idx, e_begin, E_local, C) == (slot_row >= 0)).all()
+
+
+def test_capacity_layout_without_drops_matches_offsets_layout():
+    """With C >= every expert count nothing is dropped: ranks and layer output are those of the
+    monotone-offsets layout, rows moved to e*C + rank."""
+    sh = wl.MoEShape(T=30, d=16, E=8, top_k=2, F=8, E_local=4, e_begin=2, F_shared=8)
+    inp = wl.custom_inputs(sh, seed=6)
+    plain = oracle.layer_forward(inp)
+    C = int(plain["counts"].max())
+    capped = oracle.layer_forward(dict(inp, shape=sh.replace(expert_capacity=C)))
+    np.testing.assert_array_equal(capped["out"], plain["out"])
+    le = oracle.local_expert(plain["topk_idx"], sh.e_begin, sh.E_local)
+    rank = plain["slot_row"] - np.where(le >= 0, plain["offsets"][np.maximum(le, 0)], 0)
+    np.testing.assert_array_equal(capped["slot_row"], np.where(le >= 0, le * C + rank, -1))
+
+
+def test_capacity_layer_output_by_loops():
+    """Layer with drops (capacity 1) against per-token loops: a dropped slot contributes nothing."""
+    sh = wl.MoEShape(T=10, d=8, E=4, top_k=2, F=6, E_local=4, expert_capacity=1)
+    inp = wl.custom_inputs(sh, seed=8)
+    res = oracle.layer_forward(inp)
+    xd = oracle.bf16_to_f64(inp["x"])
+    taken = [0] * 4
+    for t in range(10):
+        out = np.zeros(8)
+        for j in range(2):
+            e = int(res["topk_idx"][t, j])
+            if taken[e] < 1:
+                out += res["topk_w"][t, j] * _dense_swiglu_loops(
+                    xd[t:t + 1], oracle.bf16_to_f64(inp["w13"][e]), oracle.bf16_to_f64(inp["w2"][e]))[0]
+            taken[e] += 1
+        np.testing.assert_allclose(res["out"][t], out, rtol=1e-11, atol=1e-12)
+    assert sum(taken) == 20 and (res["slot_row"] >= 0).sum() == 4
+
+
 # ----------------------------------------------------------------------------------------
 # SwiGLU expert MLP, combine and the layer
 # ----------------------------------------------------------------------------------------
