@@ -158,6 +158,61 @@ def crossover_run():
     return rows
 
 
+def masked_decode_run(workload, capacity):
+    """One decode step in the offsets layout and in the masked-decode layout (equal segments of
+    `capacity` rows per local expert; capacity T keeps every slot), each called eagerly and
+    replayed from a HIP graph captured once.  Per-call times follow the paper's protocol (warmup
+    10, 200 calls per round under 100 us else 50, median of 3 round medians); the HBM figure
+    counts the weights of the experts that received rows, the shared-expert and router weights,
+    token rows in and out and the routing arrays."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    base = wl.make_inputs(workload)
+    sh0 = base["shape"]
+    C = capacity if capacity > 0 else sh0.T
+    rows, outs, dropped = [], {}, 0
+    for name, sh in (("offsets", sh0), ("masked", sh0.replace(expert_capacity=C))):
+        layer = moe.DeviceLayer(dict(base, shape=sh), device="cuda:0")
+        layer.forward()
+        torch.cuda.synchronize()
+        t_eager = timed_median(layer.forward, 50)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            layer.forward()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            layer.forward()
+        t_graph = timed_median(g.replay, 50)
+        g.replay()
+        torch.cuda.synchronize()
+        outs[name] = moe.bf16_bits(layer.out)
+        counts = layer.region(moe.MOE_REGION_COUNTS, torch.int32, (sh.E_local,)).cpu().numpy()
+        d, F, Fs, T, k = sh.d, sh.F, sh.F_shared, sh.T, sh.top_k
+        active = int((counts > 0).sum())
+        layer_bytes = (active * 3 * d * F * 2 + 3 * d * Fs * 2 + sh.E * d * 2 + 2 * T * d * 2 + T * k * 8)
+        kept = int(np.minimum(counts, C).sum()) if sh.expert_capacity > 0 else int(counts.sum())
+        dropped = max(dropped, int(counts.sum()) - kept)
+        rows.append({"layout": name, "expert_capacity": sh.expert_capacity, "buffer_rows": sh.capacity,
+                     "local_rows": kept, "active_local_experts": active,
+                     "eager_us": t_eager * 1e3, "graph_us": t_graph * 1e3,
+                     "graph_tokens_per_s": T / (t_graph * 1e-3),
+                     "graph_hbm_gbs": layer_bytes / (t_graph * 1e-3) / 1e9,
+                     "eager_hbm_gbs": layer_bytes / (t_eager * 1e-3) / 1e9})
+        log(f"{name}: eager {t_eager * 1e3:.1f} us, graph replay {t_graph * 1e3:.1f} us, "
+            f"{rows[-1]['graph_hbm_gbs']:.0f} GB/s")
+        del g, layer
+        torch.cuda.empty_cache()
+    # with no slot dropped both layouts compute the same rows with the same tiles
+    same = bool(np.array_equal(outs["offsets"], outs["masked"])) if dropped == 0 else None
+    return sh0, C, rows, same
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -193,6 +248,11 @@ def main():
     ap.add_argument("--crossover", action="store_true",
                     help="the paper's RQ4 kernel-crossover sweep (E=64, d=2048, F=1408, top-2, 8 local experts, "
                          "me = tokens per expert) instead of the layer benchmark")
+    ap.add_argument("--masked-decode", action="store_true",
+                    help="one decode step of --workload (default k2decode) in the offsets and the masked-decode "
+                         "layout, eager and replayed from a HIP graph, instead of the layer benchmark")
+    ap.add_argument("--capacity", type=int, default=0,
+                    help="expert capacity of --masked-decode (0: T, every slot kept)")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (reference dispatch for HBM counters)")
     args = ap.parse_args()
@@ -216,6 +276,21 @@ def main():
                           "data": "synthetic", "vs_baseline": None,
                           "protocol": "warmup 10; 200 calls per round for me < 16 else 50; median of 3 round "
                                       "medians; HIP events on the library's stream",
+                          "rows": rows}), flush=True)
+        return
+    if args.masked_decode:
+        workload = args.workload if args.workload != "dsv3" else "k2decode"
+        sh0, C, rows, same = masked_decode_run(workload, args.capacity)
+        print(json.dumps({"metric": "decode-step MoE-layer latency and HBM GB/s, offsets vs masked-decode layout, "
+                                    "eager vs HIP-graph replay, 1 MI355X",
+                          "unit": "us", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "config": {"workload": workload, "T": sh0.T, "d": sh0.d, "E": sh0.E, "top_k": sh0.top_k,
+                                     "E_local": sh0.E_local, "F": sh0.F, "F_shared": sh0.F_shared,
+                                     "expert_capacity": C},
+                          "protocol": "warmup 10; 50 calls per round; median of 3 round medians; HIP events on "
+                                      "the capturing stream",
+                          "masked_equals_offsets_output": same,
                           "rows": rows}), flush=True)
         return
     log(f"generating inputs of workload {args.workload}")

@@ -54,6 +54,13 @@
  *    ws13/ws2   [2F_s, d] / [d, F_s]     shared expert (same packing), applied to every token with weight 1
  *    out        [T, d]             bf16
  *  with cap = T * min(top_k, E_local), the most local rows a batch can produce.
+ *
+ *  Masked-decode layout (shape->expert_capacity = C > 0; the equal-stride capacity
+ *  offsets plus valid counts of the paper's kernel-generation section): cap = E_local * C,
+ *  local expert e owns rows [e C, e C + min(counts[e], C)) and offsets[e] = e C; counts[e]
+ *  stays the number of slots routed to e, of which the first C (ascending token) are kept
+ *  and the others dropped (slot_row = -1, no routed contribution).  Every buffer size and
+ *  every launch shape then depends on the shape only, not on the routing.
  */
 #ifndef MOE_MI355X_H
 #define MOE_MI355X_H
@@ -65,7 +72,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 1
+#define MOE_ABI_VERSION 2
 
 typedef enum moe_status {
   MOE_OK = 0,
@@ -125,6 +132,10 @@ typedef struct moe_shape {
   int32_t topk_group;   /* groups kept per token when n_group > 1       */
   int32_t renormalize;  /* 0 or 1                                       */
   float routed_scale;   /* multiplies every routed gate                 */
+  int32_t expert_capacity; /* 0: rows of all local experts packed by the monotone
+                              [E_local+1] offsets; C > 0: masked-decode layout, expert e
+                              owns the equal-stride segment [e C, e C + C) and keeps its
+                              first C slots (ascending token), later slots are dropped */
 } moe_shape_t;
 
 /* Library ABI version (MOE_ABI_VERSION of the build). */
@@ -159,6 +170,9 @@ int moe_route(const moe_shape_t* shape, const void* x, const void* w_router, con
  * writes counts and the monotone offsets (expert e owns rows [offsets[e], offsets[e+1])),
  * orders the rows of one expert by ascending token (a stable counting sort), writes
  * row_token and slot_row, and gathers x_perm[r] = x[row_token[r]] (bit-exact copy).
+ * Masked-decode layout (expert_capacity C > 0): offsets[e] = e C, rows e C + rank for the
+ * slots ranked below C, the others dropped; row_token and x_perm are written for the kept
+ * rows only.
  * ws: MOE_WS_PERMUTE bytes. */
 int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x,
                 int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* slot_row,
@@ -168,8 +182,11 @@ int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x
  * [offsets[e], offsets[e+1]):  y_perm[r] = W2_e (silu(W1_e x_perm[r]) * (W3_e x_perm[r])).
  * The activation is rounded to bf16 before the second GEMM; accumulation is float32.
  * `offsets` is a device array of E_local + 1 entries (e.g. from moe_permute) and must
- * satisfy 0 = offsets[0] <= ... <= offsets[E_local] <= cap.  The shared expert is this
- * call with E_local = 1, F = F_shared and offsets = {0, T} over x.
+ * satisfy 0 = offsets[0] <= ... <= offsets[E_local] <= cap (entries are clamped to [0, cap]).
+ * Masked-decode layout (expert_capacity C > 0): `offsets` is instead the device array of the
+ * E_local per-expert counts (e.g. moe_permute's `counts`); expert e runs rows
+ * [e C, e C + min(counts[e], C)).  The shared expert is this call with E_local = 1,
+ * F = F_shared, expert_capacity = 0 and offsets = {0, T} over x.
  * ws: MOE_WS_FFN bytes. */
 int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets,
                     const void* w13, const void* w2, void* y_perm,

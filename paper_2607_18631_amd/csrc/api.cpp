@@ -34,7 +34,10 @@ int ok() {
 constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+// rows of the expert-ordered buffers: every local slot (offsets layout) or E_local equal
+// segments of expert_capacity rows (masked-decode layout)
 int64_t capacity(const moe_shape_t* s) {
+  if (s->expert_capacity > 0) return (int64_t)s->E_local * s->expert_capacity;
   return s->T * (int64_t)(s->top_k < s->E_local ? s->top_k : s->E_local);
 }
 
@@ -73,6 +76,10 @@ int check_shape(const moe_shape_t* s) {
   if (s->renormalize != 0 && s->renormalize != 1)
     return fail(MOE_ERR_INVALID_ARG, "renormalize (%d) is not 0 or 1", s->renormalize);
   if (!std::isfinite(s->routed_scale)) return fail(MOE_ERR_INVALID_ARG, "routed_scale is not finite");
+  if (s->expert_capacity < 0) return fail(MOE_ERR_INVALID_ARG, "expert_capacity (%d) < 0", s->expert_capacity);
+  if ((int64_t)s->E_local * s->expert_capacity >= (int64_t(1) << 31))
+    return fail(MOE_ERR_UNSUPPORTED, "E_local * expert_capacity (%lld) >= 2^31",
+                (long long)((int64_t)s->E_local * s->expert_capacity));
   return MOE_OK;
 }
 
@@ -226,6 +233,7 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
   p.slot_row = slot_row;
   p.x_perm = static_cast<moe::bf16_t*>(x_perm);
   p.cap = capacity(s);
+  p.expert_capacity = s->expert_capacity;
   p.blk_count = static_cast<int32_t*>(ws);
   p.blk_base = at<int32_t>(ws, ws_permute(s) / 2);
   return hip_status(moe::launch_permute(p, st, mark ? mark_permute : nullptr),
@@ -242,6 +250,9 @@ struct SharedOperands {
   int64_t T = 0;
 };
 
+// `offsets`: the monotone [groups + 1] row offsets, or with seg_stride > 0 the [groups]
+// row counts of equal segments of seg_stride rows (masked-decode layout).
+//
 // Gathered rows for the up-projection: row r of the grouped part is token row_index[r] of X
 // (X has x_rows rows); row_index == nullptr means X is already in expert order.
 struct Gather {
@@ -251,8 +262,10 @@ struct Gather {
 
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
            int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0,
-           const SharedOperands* sh = nullptr, Gather gather = Gather{}, int64_t rows_hint = 0) {
+           const SharedOperands* sh = nullptr, Gather gather = Gather{}, int64_t rows_hint = 0,
+           int seg_stride = 0) {
   moe::GemmProblem up{};
+  up.seg_stride = seg_stride;
   up.rows_hint = rows_hint > 0 ? rows_hint : (groups > 0 ? (rows + groups - 1) / groups : rows);
   up.X = static_cast<const moe::bf16_t*>(X);
   up.row_index = gather.row_index;
@@ -397,7 +410,7 @@ int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t*
   CHECK(check_ptr(y_perm, 16, "y_perm"));
   CHECK(check_ws(shape, MOE_WS_FFN, ws, ws_bytes));
   CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, ws, y_perm,
-               as_stream(stream)));
+               as_stream(stream), nullptr, 0, nullptr, Gather{}, 0, shape->expert_capacity));
   return ok();
 }
 
@@ -479,11 +492,14 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     gather.row_index = row_token;
     gather.x_rows = shape->T;
   }
-  // expected rows per local expert (uniform routing): T * top_k / E
-  const int64_t rows_hint = std::max<int64_t>(1, shape->T * shape->top_k / shape->E);
-  CHECK(do_ffn(fused_gather ? x : x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F,
-               at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN, merged ? &so : nullptr, gather,
-               rows_hint));
+  // expected rows per local expert (uniform routing): T * top_k / E, at most the capacity
+  int64_t rows_hint = std::max<int64_t>(1, shape->T * shape->top_k / shape->E);
+  const int C = shape->expert_capacity;
+  if (C > 0) rows_hint = std::min<int64_t>(rows_hint, C);
+  // the masked-decode layout hands the GEMM the per-expert counts and the segment stride
+  CHECK(do_ffn(fused_gather ? x : x_perm, C > 0 ? counts : offsets, shape->E_local, capacity(shape), w13, w2,
+               shape->d, shape->F, at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN,
+               merged ? &so : nullptr, gather, rows_hint, C));
   if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
   if (shape->F_shared > 0 && !merged)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,

@@ -130,8 +130,11 @@ struct TileSpace {
   int groups, tiles_n, tiles_x, total;
   int base_total;            // (m, n) tiles
   int nk, kchunk;            // K slices; slices per chunk
-  const int* s_off;          // [groups + 1] row offsets clamped to [0, max_rows]
+  int seg_stride;            // > 0: group g owns rows [g * seg_stride, g * seg_stride + s_off[g])
+  const int* s_off;          // [groups + 1] row offsets clamped to [0, max_rows] (or valid lengths)
   const int* s_tp;           // [groups + 1] first tile of each group; s_tp[groups] = grouped tiles
+  __device__ int seg_begin(int g) const { return seg_stride > 0 ? g * seg_stride : s_off[g]; }
+  __device__ int seg_end(int g) const { return seg_stride > 0 ? g * seg_stride + s_off[g] : s_off[g + 1]; }
 };
 
 // Build the launch's tile table in LDS (every thread of the block calls this).
@@ -141,7 +144,13 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
   TileSpace ts;
   ts.tiles_n = (p.N + outn - 1) / outn;
   int groups = p.groups;
-  if (p.offsets) {
+  ts.seg_stride = 0;
+  if (p.offsets && p.seg_stride > 0) {
+    // equal-stride segments: the valid length of each, clamped to [0, seg_stride] (the
+    // launcher keeps groups * seg_stride <= max_rows)
+    ts.seg_stride = p.seg_stride;
+    for (int g = tid; g < groups; g += NTH) s_off[g] = min(max(p.offsets[g], 0), p.seg_stride);
+  } else if (p.offsets) {
     // clamp to [0, max_rows]: any offsets content keeps every access inside the buffers
     const int cap = (int)p.max_rows;
     for (int g = tid; g <= groups; g += NTH) s_off[g] = min(max(p.offsets[g], 0), cap);
@@ -156,7 +165,7 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     int g = tid * PER + i;
-    int m = g < groups ? max(s_off[g + 1] - s_off[g], 0) : 0;
+    int m = g >= groups ? 0 : ts.seg_stride > 0 ? s_off[g] : max(s_off[g + 1] - s_off[g], 0);
     loc[i] = ((m + BM - 1) / BM) * ts.tiles_n;
     lsum += loc[i];
   }
@@ -228,8 +237,8 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
       if (ts.s_tp[mid] <= t) lo = mid; else hi = mid;
     }
     const int g = __builtin_amdgcn_readfirstlane(lo);
-    row0g = __builtin_amdgcn_readfirstlane(ts.s_off[g]);
-    d.row_end = __builtin_amdgcn_readfirstlane(ts.s_off[g + 1]);
+    row0g = __builtin_amdgcn_readfirstlane(ts.seg_begin(g));
+    d.row_end = __builtin_amdgcn_readfirstlane(ts.seg_end(g));
     local = t - __builtin_amdgcn_readfirstlane(ts.s_tp[g]);
     d.W = p.W + (int64_t)g * p.w_group_stride;
     d.X = p.X;
@@ -762,6 +771,9 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   if (p.ksplit > 1 && (p.epi != EPI_F32 || p.offsets != nullptr || p.rows2 > 0)) return hipErrorInvalidValue;
   // gathered rows: the per-lane 32-bit source offsets must reach every row of X
   if (p.row_index && (p.x_rows < 1 || p.x_rows * p.ldx * 2 >= (int64_t(1) << 32))) return hipErrorInvalidValue;
+  // equal-stride segments must fit the row bound
+  if (p.seg_stride > 0 && (p.offsets == nullptr || (int64_t)p.groups * p.seg_stride > p.max_rows))
+    return hipErrorInvalidValue;
   // 256 x 256 tiles, 8 waves, two 64-wide K slices in flight: the best measured on the DeepSeek-V3,
   // Mixtral and skewed workloads (largest reuse per byte copied into LDS; also whenever a large
   // dense extra group shares the launch).  With few expected rows per group the launch is a

@@ -18,7 +18,8 @@ enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2 };
 struct GemmProblem {
   const bf16_t* X;            // token rows, row stride ldx (elements)
   int64_t ldx;
-  const int32_t* offsets;     // device [groups+1]; nullptr = one group of rows_single rows
+  const int32_t* offsets;     // device [groups+1]; nullptr = one group of rows_single rows;
+                              // with seg_stride > 0: device [groups] row counts
   int32_t groups;
   int64_t rows_single;
   int64_t max_rows;           // host-known bound of offsets[groups] (grid sizing only)
@@ -46,6 +47,9 @@ struct GemmProblem {
   // expected rows per group (0 = unknown): selects the tile shape (the row counts themselves
   // stay on the device)
   int64_t rows_hint;
+  // equal-stride segments (masked-decode layout): group g owns rows
+  // [g * seg_stride, g * seg_stride + min(offsets[g], seg_stride)); 0 = monotone offsets
+  int32_t seg_stride;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
@@ -80,6 +84,7 @@ struct PermuteProblem {
   int32_t* slot_row;          // [T, top_k]
   bf16_t* x_perm;             // [cap, d]; nullptr: no row copy (the GEMM gathers the rows itself)
   int64_t cap;                // rows of row_token / x_perm
+  int32_t expert_capacity;    // > 0: masked-decode layout (rows e * C + rank, rank < C)
   int32_t* blk_count;         // workspace [nblk, E_local]
   int32_t* blk_base;          // workspace [nblk, E_local]
 };

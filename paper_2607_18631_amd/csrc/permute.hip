@@ -13,6 +13,9 @@
 //                  rows (read once, written k_local times, 16-byte vectors); skipped when
 //                  the caller's GEMM reads the token rows through row_token itself
 //
+// Masked-decode layout (expert capacity C > 0): expert e's rows are e * C + rank for the
+// ranks below C; later slots are dropped (slot_row = -1) and offsets[e] = e * C.
+//
 // The in-chunk rank uses wavefront ballots instead of atomics, so the order inside an
 // expert is ascending token (a stable counting sort) and run-to-run identical: for every
 // slot column j' and every bit b of the local expert id, one ballot gives the lanes whose
@@ -117,7 +120,8 @@ __global__ __launch_bounds__(64 * RW) void k_rank(PermuteProblem p) {
     if (tid == 0) s_off[E_local] = tot;
     __syncthreads();
     if (c == 0)
-      for (int e = tid; e <= E_local; e += 64 * RW) p.offsets[e] = s_off[e];
+      for (int e = tid; e <= E_local; e += 64 * RW)
+        p.offsets[e] = p.expert_capacity > 0 ? e * p.expert_capacity : s_off[e];
   }
   if (wave >= k) return;                       // wave-uniform
 
@@ -168,7 +172,13 @@ __global__ __launch_bounds__(64 * RW) void k_rank(PermuteProblem p) {
     const int j = wave + m * RW;
     if (j >= k) break;
     int row = -1;
-    if (myle[j] >= 0) row = s_off[myle[j]] + base[myle[j]] + rank[m];
+    if (myle[j] >= 0) {
+      const int grank = base[myle[j]] + rank[m];             // rank inside the expert
+      if (p.expert_capacity > 0)                             // masked-decode layout: drop past C
+        row = grank < p.expert_capacity ? myle[j] * p.expert_capacity + grank : -1;
+      else
+        row = s_off[myle[j]] + grank;
+    }
     if (row >= p.cap) row = -1;              // unreachable for a consistent histogram; keeps writes in bounds
     p.slot_row[t * k + j] = row;
     if (row >= 0) p.row_token[row] = (int32_t)t;

@@ -34,7 +34,8 @@ class MoEShapeC(ctypes.Structure):
                 ("top_k", ctypes.c_int32), ("e_begin", ctypes.c_int32), ("E_local", ctypes.c_int32),
                 ("F", ctypes.c_int32), ("F_shared", ctypes.c_int32), ("gate", ctypes.c_int32),
                 ("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32),
-                ("renormalize", ctypes.c_int32), ("routed_scale", ctypes.c_float)]
+                ("renormalize", ctypes.c_int32), ("routed_scale", ctypes.c_float),
+                ("expert_capacity", ctypes.c_int32)]
 
 
 class MoEError(RuntimeError):
@@ -79,7 +80,7 @@ def lib():
 
 def shape_c(sh: MoEShape) -> MoEShapeC:
     return MoEShapeC(sh.T, sh.d, sh.E, sh.top_k, sh.e_begin, sh.E_local, sh.F, sh.F_shared, sh.gate,
-                     sh.n_group, sh.topk_group, sh.renormalize, sh.routed_scale)
+                     sh.n_group, sh.topk_group, sh.renormalize, sh.routed_scale, sh.expert_capacity)
 
 
 def last_error() -> str:

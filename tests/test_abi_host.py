@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(moe.EXPORTS), names
     for n in names:
         assert hasattr(L, n), n
-    assert L.moe_abi_version() == 1
+    assert L.moe_abi_version() == 2
 
 
 def test_status_strings():
@@ -38,6 +38,18 @@ def test_status_strings():
     for s in range(5):
         assert L.moe_status_string(s).decode().startswith(
             ["MOE_OK", "MOE_ERR_INVALID_ARG", "MOE_ERR_UNSUPPORTED", "MOE_ERR_WORKSPACE", "MOE_ERR_HIP"][s])
+
+
+def test_masked_layout_workspace():
+    """The masked-decode layout sizes the permuted buffers by E_local * C rows."""
+    C = 5
+    sh = BASE.replace(expert_capacity=C)
+    cap = sh.E_local * C
+    assert sh.capacity == cap
+    off = [moe.workspace_offset(sh, r) for r in range(9)]
+    assert off[moe.MOE_REGION_X_PERM] - off[moe.MOE_REGION_ROW_TOKEN] >= cap * 4
+    assert off[moe.MOE_REGION_Y_PERM] - off[moe.MOE_REGION_X_PERM] >= cap * sh.d * 2
+    assert moe.workspace_size(sh, moe.MOE_WS_FFN) >= cap * sh.F * 2
 
 
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))
@@ -89,6 +101,8 @@ BASE = wl.MoEShape(T=64, d=64, E=8, top_k=2, F=64, E_local=8)
     (BASE.replace(routed_scale=float("nan")), moe.MOE_ERR_INVALID_ARG, "routed_scale"),
     (BASE.replace(T=-1), moe.MOE_ERR_INVALID_ARG, "T (-1) < 0"),
     (BASE.replace(T=2 ** 30, top_k=2), moe.MOE_ERR_UNSUPPORTED, "T * top_k"),
+    (BASE.replace(expert_capacity=-1), moe.MOE_ERR_INVALID_ARG, "expert_capacity (-1) < 0"),
+    (BASE.replace(expert_capacity=2 ** 28), moe.MOE_ERR_UNSUPPORTED, "E_local * expert_capacity"),
 ])
 def test_shape_validation(sh, status, needle):
     st, msg = _layer_call(sh)
