@@ -213,6 +213,39 @@ def masked_decode_run(workload, capacity):
     return sh0, C, rows, same
 
 
+def fusion_matrix_run(workload, steps):
+    """The layer in the paper's four kernel structures (fuse_gather x fuse_combine): per-call
+    time (warmup 10, median of 3 round medians of `steps` calls) and the per-step split of one
+    traced pass per call, averaged."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    base = wl.make_inputs(workload)
+    sh0 = base["shape"]
+    ev = HipEvents()
+    nstep = len(moe.MOE_STEP_NAMES)
+    rows = []
+    for name, fusion in wl.FUSION_VARIANTS.items():
+        sh = sh0.replace(fusion=fusion)
+        layer = moe.DeviceLayer(dict(base, shape=sh), device="cuda:0")
+        t = timed_median(layer.forward, steps)
+        events = [ev.create(nstep + 1) for _ in range(steps)]
+        for i in range(steps):
+            layer.forward_traced(events[i])
+        torch.cuda.synchronize()
+        split = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in events]).mean(axis=0)
+        for e in events:
+            ev.destroy(e)
+        rows.append({"variant": name, "fusion": fusion, "layer_us": t * 1e3, "tokens_per_s": sh.T / (t * 1e-3),
+                     "step_us": {n: round(float(split[i]) * 1e3, 2) for i, n in enumerate(moe.MOE_STEP_NAMES)}})
+        log(f"{name}: {t * 1e3:.1f} us per layer")
+        del layer
+        torch.cuda.empty_cache()
+    return sh0, rows
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -251,6 +284,8 @@ def main():
     ap.add_argument("--masked-decode", action="store_true",
                     help="one decode step of --workload (default k2decode) in the offsets and the masked-decode "
                          "layout, eager and replayed from a HIP graph, instead of the layer benchmark")
+    ap.add_argument("--fusion-matrix", action="store_true",
+                    help="time the layer of --workload in the four fuse_gather x fuse_combine structures")
     ap.add_argument("--capacity", type=int, default=0,
                     help="expert capacity of --masked-decode (0: T, every slot kept)")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
@@ -291,6 +326,18 @@ def main():
                           "protocol": "warmup 10; 50 calls per round; median of 3 round medians; HIP events on "
                                       "the capturing stream",
                           "masked_equals_offsets_output": same,
+                          "rows": rows}), flush=True)
+        return
+    if args.fusion_matrix:
+        sh0, rows = fusion_matrix_run(args.workload, max(args.steps, 10))
+        print(json.dumps({"metric": "MoE-layer latency per kernel structure (fuse_gather x fuse_combine), 1 MI355X",
+                          "unit": "us", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "config": {"workload": args.workload, "T": sh0.T, "d": sh0.d, "E": sh0.E,
+                                     "top_k": sh0.top_k, "E_local": sh0.E_local, "F": sh0.F,
+                                     "F_shared": sh0.F_shared},
+                          "protocol": "warmup 10; median of 3 round medians of the per-call event times; step "
+                                      "split from traced calls",
                           "rows": rows}), flush=True)
         return
     log(f"generating inputs of workload {args.workload}")

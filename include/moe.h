@@ -34,7 +34,8 @@
  *    T == 0 is a valid no-op.  Results for inputs holding Inf or NaN are
  *    unspecified.
  *  - Determinism.  Every output is bit-identical from run to run (no floating-
- *    point atomics anywhere).
+ *    point atomics), except moe_layer_forward with MOE_FUSE_COMBINE, whose expert
+ *    rows are added into the token rows with float32 atomics in no fixed order.
  *
  * Layouts
  * -------
@@ -72,7 +73,16 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 2
+#define MOE_ABI_VERSION 3
+
+/* moe_shape_t.fusion: which of the paper's four kernel structures moe_layer_forward runs
+ * (Section 4, kernel generation: fuse_gather folds the token permute into the first GEMM's
+ * prologue, fuse_combine folds the weighted combine into the second GEMM's epilogue).
+ * 0 = the library's choice (gather folded where its 32-bit row offsets reach all of x,
+ * combine separate); otherwise MOE_FUSION_SET | any of MOE_FUSE_GATHER, MOE_FUSE_COMBINE. */
+#define MOE_FUSION_SET 0x10
+#define MOE_FUSE_GATHER 0x1
+#define MOE_FUSE_COMBINE 0x2
 
 typedef enum moe_status {
   MOE_OK = 0,
@@ -105,10 +115,11 @@ typedef enum moe_ws_region {
   MOE_REGION_OFFSETS = 3,    /* i32 [E_local+1]  */
   MOE_REGION_ROW_TOKEN = 4,  /* i32 [cap]        */
   MOE_REGION_SLOT_ROW = 5,   /* i32 [T, top_k]   */
-  MOE_REGION_X_PERM = 6,     /* bf16 [cap, d]; written by moe_layer_forward only when T * d * 2 >= 2^32
-                                (otherwise the up-projection reads x through row_token) */
-  MOE_REGION_Y_PERM = 7,     /* bf16 [cap, d]    */
-  MOE_REGION_SHARED_Y = 8,   /* bf16 [T, d] (only when F_shared > 0) */
+  MOE_REGION_X_PERM = 6,     /* bf16 [cap, d]; written by moe_layer_forward only when the gather is
+                                not folded (the up-projection otherwise reads x through row_token) */
+  MOE_REGION_Y_PERM = 7,     /* bf16 [cap, d]; not written when the combine is folded */
+  MOE_REGION_SHARED_Y = 8,   /* bf16 [T, d] (only when F_shared > 0; not written when the
+                                combine is folded) */
   MOE_REGION_COUNT_ = 9
 } moe_ws_region_t;
 
@@ -136,6 +147,8 @@ typedef struct moe_shape {
                               [E_local+1] offsets; C > 0: masked-decode layout, expert e
                               owns the equal-stride segment [e C, e C + C) and keeps its
                               first C slots (ascending token), later slots are dropped */
+  int32_t fusion;       /* moe_layer_forward's kernel structure: 0 or MOE_FUSION_SET | flags
+                           (see MOE_FUSE_GATHER / MOE_FUSE_COMBINE); ignored by the other calls */
 } moe_shape_t;
 
 /* Library ABI version (MOE_ABI_VERSION of the build). */
@@ -201,10 +214,17 @@ int moe_combine(const moe_shape_t* shape, const void* y_perm, const int32_t* slo
                 const float* topk_w, const void* shared_y, void* out, void* stream);
 
 /* The whole layer: route -> permute -> grouped_ffn (+ shared expert) -> combine.
- * The row copy of the permutation is folded into the up-projection (the paper's gathered
- * first GEMM, Section 3.1): its token rows are read from x through row_token, so x_perm is
- * not materialised (when T * d * 2 < 2^32; larger batches copy the rows first).  Results
- * are identical either way.
+ * Kernel structure (shape->fusion; Section 3.1 kernel sub-plan, Section 4 kernel generation):
+ *  - gather folded (MOE_FUSE_GATHER, and the default when T * d * 2 < 2^32): the
+ *    up-projection reads its token rows from x through row_token, x_perm is not written;
+ *    unfolded, the permutation copies the rows into x_perm first.  Results are identical.
+ *    An explicit MOE_FUSE_GATHER with T * d * 2 >= 2^32 is MOE_ERR_UNSUPPORTED.
+ *  - combine folded (MOE_FUSE_COMBINE): the down-projection's epilogue adds
+ *    topk_w * (expert row, float32) into a float32 [T, d] accumulator with atomics (the shared
+ *    expert's rows with weight 1), and one pass rounds it to bf16; y_perm and shared_y are not
+ *    written.  The expert rows are not rounded to bf16 first, and the order of the additions
+ *    is not fixed, so results may differ from run to run in the last bf16 bit.
+ *  Default (fusion = 0): gather folded where allowed, combine separate.
  * ws13 / ws2 are required when F_shared > 0 and ignored otherwise.
  * ws: MOE_WS_LAYER bytes; its named regions hold the intermediates afterwards. */
 int moe_layer_forward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,

@@ -80,7 +80,18 @@ int check_shape(const moe_shape_t* s) {
   if ((int64_t)s->E_local * s->expert_capacity >= (int64_t(1) << 31))
     return fail(MOE_ERR_UNSUPPORTED, "E_local * expert_capacity (%lld) >= 2^31",
                 (long long)((int64_t)s->E_local * s->expert_capacity));
+  if (s->fusion != 0 && (!(s->fusion & MOE_FUSION_SET) ||
+                         (s->fusion & ~(MOE_FUSION_SET | MOE_FUSE_GATHER | MOE_FUSE_COMBINE))))
+    return fail(MOE_ERR_INVALID_ARG, "fusion (0x%x) is neither 0 nor MOE_FUSION_SET | MOE_FUSE_* flags", s->fusion);
   return MOE_OK;
+}
+
+// the up-projection reads token rows through row_token (per-lane 32-bit offsets into x)
+bool gather_fits(const moe_shape_t* s) { return s->T * (int64_t)s->d * 2 < (int64_t(1) << 32); }
+bool fuse_gather(const moe_shape_t* s) {
+  return s->fusion == 0 ? gather_fits(s) : (s->fusion & MOE_FUSE_GATHER) != 0;
+}
+bool fuse_combine(const moe_shape_t* s) { return (s->fusion & MOE_FUSE_COMBINE) != 0;
 }
 
 int check_ptr(const void* p, size_t align, const char* name) {
@@ -108,7 +119,9 @@ size_t ws_ffn(const moe_shape_t* s) { return align_up((size_t)capacity(s) * s->F
 
 struct LayerLayout {
   size_t region[MOE_REGION_COUNT_];
-  size_t logits, perm_ws, act, act_s, total;
+  size_t logits, perm_ws, act, act_s;
+  size_t acc32, row_weight;   // combine folded into the down-projection only
+  size_t total;
 };
 
 LayerLayout layer_layout(const moe_shape_t* s) {
@@ -133,6 +146,8 @@ LayerLayout layer_layout(const moe_shape_t* s) {
   L.perm_ws = take(ws_permute(s));
   L.act = take(ws_ffn(s));
   L.act_s = take(s->F_shared > 0 ? T * (size_t)s->F_shared * 2 : 0);
+  L.acc32 = take(fuse_combine(s) ? T * d * 4 : 0);
+  L.row_weight = take(fuse_combine(s) ? cap * 4 : 0);
   L.total = off;
   return L;
 }
@@ -218,7 +233,7 @@ int do_route(const moe_shape_t* s, const void* x, const void* w_router, const fl
 
 int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int32_t* counts, int32_t* offsets,
                int32_t* row_token, int32_t* slot_row, void* x_perm, void* ws, hipStream_t st,
-               Marker mark = nullptr) {
+               Marker mark = nullptr, const float* topk_w = nullptr, float* row_weight = nullptr) {
   moe::PermuteProblem p{};
   p.topk_idx = topk_idx;
   p.x = static_cast<const moe::bf16_t*>(x);
@@ -234,6 +249,8 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
   p.x_perm = static_cast<moe::bf16_t*>(x_perm);
   p.cap = capacity(s);
   p.expert_capacity = s->expert_capacity;
+  p.topk_w = topk_w;
+  p.row_weight = row_weight;
   p.blk_count = static_cast<int32_t*>(ws);
   p.blk_base = at<int32_t>(ws, ws_permute(s) / 2);
   return hip_status(moe::launch_permute(p, st, mark ? mark_permute : nullptr),
@@ -260,10 +277,20 @@ struct Gather {
   int64_t x_rows = 0;
 };
 
+// The combine folded into the down-projection: rows are added, times their gate, into the
+// float32 token rows acc [rows, d] (token[r] / weight[r] of the grouped rows; null = the row
+// itself / 1; the shared expert's rows always the row itself with weight 1).
+struct Scatter {
+  float* acc = nullptr;
+  const int32_t* token = nullptr;
+  const float* weight = nullptr;
+  int64_t rows = 0;
+};
+
 int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, const void* w13, const void* w2,
            int d, int F, void* act, void* y, hipStream_t st, Marker mark = nullptr, int down_step = 0,
            const SharedOperands* sh = nullptr, Gather gather = Gather{}, int64_t rows_hint = 0,
-           int seg_stride = 0) {
+           int seg_stride = 0, Scatter scatter = Scatter{}) {
   moe::GemmProblem up{};
   up.seg_stride = seg_stride;
   up.rows_hint = rows_hint > 0 ? rows_hint : (groups > 0 ? (rows + groups - 1) / groups : rows);
@@ -307,6 +334,14 @@ int do_ffn(const void* X, const int32_t* offsets, int groups, int64_t rows, cons
     dn.W2 = static_cast<const moe::bf16_t*>(sh->w2);
     dn.Y2 = sh->y;
     dn.rows2 = (int32_t)sh->T;
+  }
+  if (scatter.acc) {
+    dn.epi = moe::EPI_SCATTER;
+    dn.Y = scatter.acc;
+    if (sh) dn.Y2 = scatter.acc;
+    dn.scatter_token = scatter.token;
+    dn.scatter_weight = scatter.weight;
+    dn.scatter_rows = scatter.rows;
   }
   return hip_status(moe::launch_grouped_gemm(dn, st), "expert down-projection launch");
 }
@@ -446,6 +481,9 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     CHECK(check_ptr(ws2, 16, "ws2"));
   }
   CHECK(check_ptr(out, 16, "out"));
+  if ((shape->fusion & MOE_FUSE_GATHER) && !gather_fits(shape))
+    return fail(MOE_ERR_UNSUPPORTED, "MOE_FUSE_GATHER needs T * d * 2 (%lld) < 2^32",
+                (long long)(shape->T * (int64_t)shape->d * 2));
   CHECK(check_ws(shape, MOE_WS_LAYER, ws, ws_bytes));
   if (events)
     for (int i = 0; i <= MOE_STEP_COUNT_; ++i)
@@ -470,10 +508,16 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
   CHECK(do_route(shape, x, w_router, bias, topk_idx, topk_w, nullptr, at<float>(ws, L.logits), st, mark));
   // the permutation folded into the up-projection's copies: its token rows are read from x
   // through row_token (no x_perm round trip), where per-lane 32-bit offsets reach all of x
-  const bool fused_gather = shape->T * (int64_t)shape->d * 2 < (int64_t(1) << 32);
+  const bool fused_gather = fuse_gather(shape);
+  // the combine folded into the down-projection: gate-weighted rows added into f32 token rows
+  const bool fused_combine = fuse_combine(shape);
+  float* acc32 = fused_combine ? at<float>(ws, L.acc32) : nullptr;
+  float* row_weight = fused_combine ? at<float>(ws, L.row_weight) : nullptr;
   if (mark) CHECK(mark(MOE_STEP_HISTOGRAM));
   CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, fused_gather ? nullptr : x_perm,
-                   at<void>(ws, L.perm_ws), st, mark));
+                   at<void>(ws, L.perm_ws), st, mark, topk_w, row_weight));
+  if (fused_combine)
+    CHECK(hip_status(moe::launch_zero_f32(acc32, shape->T * (int64_t)shape->d, st), "accumulator clear launch"));
   // a shared expert as wide as the routed ones runs inside the routed launches (its tiles
   // interleaved with the experts'), otherwise in launches of its own
   const bool merged = shape->F_shared > 0 && shape->F_shared == shape->F;
@@ -485,6 +529,11 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     so.act = at<void>(ws, L.act_s);
     so.y = shared_y;
     so.T = shape->T;
+  }
+  Scatter routed_scatter, shared_scatter;
+  if (fused_combine) {
+    routed_scatter = Scatter{acc32, row_token, row_weight, shape->T};
+    shared_scatter = Scatter{acc32, nullptr, nullptr, shape->T};
   }
   if (mark) CHECK(mark(MOE_STEP_FFN_UP));
   Gather gather;
@@ -499,15 +548,19 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
   // the masked-decode layout hands the GEMM the per-expert counts and the segment stride
   CHECK(do_ffn(fused_gather ? x : x_perm, C > 0 ? counts : offsets, shape->E_local, capacity(shape), w13, w2,
                shape->d, shape->F, at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN,
-               merged ? &so : nullptr, gather, rows_hint, C));
+               merged ? &so : nullptr, gather, rows_hint, C, routed_scatter));
   if (mark) CHECK(mark(MOE_STEP_SHARED_UP));
   if (shape->F_shared > 0 && !merged)
     CHECK(do_ffn(x, nullptr, 1, shape->T, ws13, ws2, shape->d, shape->F_shared, at<void>(ws, L.act_s), shared_y,
-                 st, mark, MOE_STEP_SHARED_DOWN));
+                 st, mark, MOE_STEP_SHARED_DOWN, nullptr, Gather{}, 0, 0, shared_scatter));
   else if (mark)
     CHECK(mark(MOE_STEP_SHARED_DOWN));
   if (mark) CHECK(mark(MOE_STEP_COMBINE));
-  CHECK(do_combine(shape, y_perm, slot_row, topk_w, shared_y, out, st));
+  if (fused_combine)
+    CHECK(hip_status(moe::launch_round_bf16(acc32, static_cast<moe::bf16_t*>(out), shape->T * (int64_t)shape->d, st),
+                     "accumulator rounding launch"));
+  else
+    CHECK(do_combine(shape, y_perm, slot_row, topk_w, shared_y, out, st));
   if (mark) CHECK(mark(MOE_STEP_COUNT_));
   g_events = nullptr;
   return ok();

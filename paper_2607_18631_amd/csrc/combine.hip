@@ -1,4 +1,5 @@
-// Gate-weighted combine: one wavefront per token, owner computes (no atomics).
+// Gate-weighted combine: one wavefront per token, owner computes (no atomics); and the
+// clear / rounding passes of the combine folded into the down-projection.
 //
 //   out[t] = bf16( sum_j topk_w[t,j] * y_perm[slot_row[t,j]]  (+ shared_y[t]) )
 //
@@ -117,7 +118,44 @@ __global__ __launch_bounds__(64 * kWaves) void k_combine(CombineProblem p) {
   }
 }
 
+// The float32 accumulator of the combine folded into the down-projection: cleared before
+// the GEMM, rounded to bf16 after it (16-byte loads and stores, grid-stride).
+__global__ __launch_bounds__(256) void k_zero_f32(float* acc, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
+    reinterpret_cast<f32x4*>(acc)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+__global__ __launch_bounds__(256) void k_round_bf16(const float* acc, bf16_t* out, int64_t n8) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
+    const f32x4 a = reinterpret_cast<const f32x4*>(acc)[2 * i];
+    const f32x4 b = reinterpret_cast<const f32x4*>(acc)[2 * i + 1];
+    u32x4 o;
+    o[0] = pack_bf16x2(a[0], a[1]);
+    o[1] = pack_bf16x2(a[2], a[3]);
+    o[2] = pack_bf16x2(b[0], b[1]);
+    o[3] = pack_bf16x2(b[2], b[3]);
+    st16(out + 8 * i, o);
+  }
+}
+
+unsigned stream_blocks(int64_t items) {
+  const int64_t b = (items + 255) / 256;
+  return (unsigned)(b < 8192 ? (b > 0 ? b : 1) : 8192);   // 32 workgroups per CU at most
+}
+
 }  // namespace
+
+hipError_t launch_zero_f32(float* acc, int64_t n, hipStream_t stream) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_zero_f32, dim3(stream_blocks(n / 4)), dim3(256), 0, stream, acc, n / 4);
+  return hipGetLastError();
+}
+
+hipError_t launch_round_bf16(const float* acc, bf16_t* out, int64_t n, hipStream_t stream) {
+  if (n % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_round_bf16, dim3(stream_blocks(n / 8)), dim3(256), 0, stream, acc, out, n / 8);
+  return hipGetLastError();
+}
 
 hipError_t launch_combine(const CombineProblem& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)((p.T + kWaves - 1) / kWaves);

@@ -37,6 +37,12 @@
 // the group's end, so the ragged last m-tile of an expert costs MFMA time in proportion to
 // its live rows (the per-expert row counts of a routed batch scatter around the mean,
 // which leaves most experts with one mostly empty m-tile).
+//
+// Variants of the same body: equal-stride row segments [g * seg_stride, + count_g) (the
+// masked-decode form of the same section: capacity offsets plus valid counts); gathered
+// token rows (the permute folded into the prologue: row r of the tile is X row
+// row_index[r]); and the scatter epilogue (the weighted combine folded into the epilogue:
+// rows added, times their gate, into float32 token rows with atomics).
 #include <type_traits>
 
 #include "common.hpp"
@@ -206,6 +212,8 @@ struct TileDesc {
   int row0, row_end, ni;
   int kb, ke, kc;            // K slices [kb, ke) of K chunk kc
   const int32_t* rows;       // gathered rows: tile row r is X row rows[row0 + r] (else row0 + r)
+  const int32_t* stok;       // EPI_SCATTER: token of each row (nullptr: the row itself)
+  const float* sw;           // EPI_SCATTER: weight of each row (nullptr: 1)
   const bf16_t* X;
   const bf16_t* W;
   void* Y;
@@ -229,6 +237,8 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
     d.X = p.X2;
     d.Y = p.Y2;
     d.rows = nullptr;
+    d.stok = nullptr;
+    d.sw = nullptr;
   } else {
     const int t = tile - x_before;                        // index among the grouped tiles
     int lo = 0, hi = ts.groups;                           // s_tp[groups] == grouped tiles > t
@@ -244,6 +254,8 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
     d.X = p.X;
     d.Y = p.Y;
     d.rows = p.row_index;
+    d.stok = p.scatter_token;
+    d.sw = p.scatter_weight;
   }
   const int mt = (d.row_end - row0g + BM - 1) / BM;
   // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
@@ -421,6 +433,60 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
           }
         }
       }
+    }
+  }
+}
+
+// EPI_SCATTER: the gate-weighted combine folded into the epilogue.  In the MFMA layout a lane
+// holds 4-column pieces of one token row, so adding the fragment straight from registers
+// would touch 32 rows (cache lines) per instruction; each 32 x 32 fragment instead goes
+// through a wave-private LDS block `lw` (32 rows of 36 floats, the padding spreads the banks)
+// and comes back two rows per instruction, 32 consecutive columns each, so every float32
+// atomic instruction covers two cache lines.  Row r of the tile adds w(r) * row into token
+// row tok(r) of Y (see TileDesc::stok / sw).
+constexpr int kScatterLd = 36;
+template <int FM, int FN>
+__device__ __forceinline__ void scatter_tile(const GemmProblem& p, const f32x16 (&acc)[FM][FN], const TileDesc& t,
+                                             int trow, int astride, int fcol, int lane, float* lw) {
+  const int hi = lane >> 5, r32 = lane & 31;
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    const int rbase = t.row0 + trow + a * astride;               // first row of the 32-row block
+    if (rbase >= t.row_end) continue;                            // wave-uniform
+    const int nrow = min(32, t.row_end - rbase);
+    // token and weight of the block's rows, one per lane (lanes 0..31)
+    int tok = -1;
+    float w = 0.f;
+    if (r32 < nrow) {
+      tok = t.stok ? t.stok[rbase + r32] : rbase + r32;
+      w = t.sw ? t.sw[rbase + r32] : 1.0f;
+      if (tok < 0 || tok >= p.scatter_rows) tok = -1;
+    }
+#pragma unroll
+    for (int b = 0; b < FN; ++b) {
+      const int col0 = fcol + b * 32;
+      if (col0 >= p.N) continue;                                 // N % 8 == 0: whole 32-col pieces or none
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 v = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]};
+        *reinterpret_cast<f32x4*>(lw + r32 * kScatterLd + 8 * q + 4 * hi) = v;
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+      const int col = col0 + r32;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int rl = 2 * j + hi;                               // block row of this lane
+        const int tj0 = __builtin_amdgcn_readlane(tok, 2 * j), tj1 = __builtin_amdgcn_readlane(tok, 2 * j + 1);
+        const float wj0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), 2 * j));
+        const float wj1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), 2 * j + 1));
+        const int tk = hi ? tj1 : tj0;
+        const float wk = hi ? wj1 : wj0;
+        const float v = lw[rl * kScatterLd + r32];
+        if (tk >= 0 && col < p.N) unsafeAtomicAdd(reinterpret_cast<float*>(t.Y) + (int64_t)tk * p.ldy + col, wk * v);
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
     }
   }
 }
@@ -616,7 +682,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       for (int s = 0; s < STAGES - 1; ++s)
         if (s < nl) issue_any(kb + s, s);
     }
-    store_tile<EPI, FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane);
+    if constexpr (EPI == EPI_SCATTER) {
+      // the last ring slot is idle until the next tile's first barrier: one LDS block per wave
+      static_assert(NW * 32 * kScatterLd * 4 <= SLICE * 2, "scatter staging fits one ring slot");
+      float* lw = reinterpret_cast<float*>(ring + (STAGES - 1) * SLICE) + wave * 32 * kScatterLd;
+      scatter_tile<FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane, lw);
+    } else {
+      store_tile<EPI, FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane);
+    }
     if (!more) break;
   }
 }
@@ -789,6 +862,13 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   switch (p.epi) {
     case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
     case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
+    case EPI_SCATTER:
+      if (p.scatter_rows < 1) return hipErrorInvalidValue;
+      switch (tier) {      // the tiers of the bf16 epilogue (same operand shapes)
+        case 20: return launch_tile<64, 128, 64, 3, 2, 2, EPI_SCATTER>(p, stream);
+        case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI_SCATTER>(p, stream);
+        default: return launch_tile<256, 256, 64, 2, 4, 2, EPI_SCATTER>(p, stream);
+      }
     case EPI_F32:
 #ifdef MOE_GEMM_SWEEP
       if (g_force_cfg[EPI_F32] >= 0) return launch_cfg<EPI_F32>(g_force_cfg[EPI_F32], p, stream);

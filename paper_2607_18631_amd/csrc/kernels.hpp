@@ -9,12 +9,15 @@ typedef uint16_t bf16_t;
 
 constexpr int kMaxGroups = 1024;  // E_local limit of the grouped GEMM's in-LDS tile table
 
-enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2 };
+enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2, EPI_SCATTER = 3 };
 
 // One grouped GEMM  Y[r, n] = sum_k X[r, k] * W_g[n, k]  for every group g and every
 // row r in [offsets[g], offsets[g+1]).  Both operands are K-contiguous.
 // EPI_SWIGLU: W_g holds 2N rows (gate rows [0,N), up rows [N,2N)) and
 //             Y[r, n] = bf16(silu(gate) * up).
+// EPI_SCATTER: float32 Y rows are token rows: Y[tok(r), n] += w(r) * (X W_g^T)[r, n] by
+//             atomics, tok(r) = scatter_token[r] and w(r) = scatter_weight[r] for the grouped
+//             rows (identity and 1 when the pointers are null, and for the extra group).
 struct GemmProblem {
   const bf16_t* X;            // token rows, row stride ldx (elements)
   int64_t ldx;
@@ -50,6 +53,10 @@ struct GemmProblem {
   // equal-stride segments (masked-decode layout): group g owns rows
   // [g * seg_stride, g * seg_stride + min(offsets[g], seg_stride)); 0 = monotone offsets
   int32_t seg_stride;
+  // EPI_SCATTER: token and gate of every grouped row; tokens outside [0, scatter_rows) are skipped
+  const int32_t* scatter_token;
+  const float* scatter_weight;
+  int64_t scatter_rows;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
@@ -85,6 +92,8 @@ struct PermuteProblem {
   bf16_t* x_perm;             // [cap, d]; nullptr: no row copy (the GEMM gathers the rows itself)
   int64_t cap;                // rows of row_token / x_perm
   int32_t expert_capacity;    // > 0: masked-decode layout (rows e * C + rank, rank < C)
+  const float* topk_w;        // [T, top_k]; read only when row_weight is set
+  float* row_weight;          // [cap] gate of each row, or nullptr
   int32_t* blk_count;         // workspace [nblk, E_local]
   int32_t* blk_base;          // workspace [nblk, E_local]
 };
@@ -104,5 +113,10 @@ struct CombineProblem {
   int32_t d, top_k;
 };
 hipError_t launch_combine(const CombineProblem& p, hipStream_t stream);
+
+// acc[0 .. n) = 0 (a fill kernel, so the call can sit inside a captured graph); n % 4 == 0
+hipError_t launch_zero_f32(float* acc, int64_t n, hipStream_t stream);
+// out[i] = bf16(acc[i]) for i < n, n % 8 == 0
+hipError_t launch_round_bf16(const float* acc, bf16_t* out, int64_t n, hipStream_t stream);
 
 }  // namespace moe

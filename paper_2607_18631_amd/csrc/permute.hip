@@ -8,7 +8,7 @@
 //                  [E_local+1] array), each slot's rank among the chunk's earlier slots
 //                  of the same expert (slot columns spread over the waves), hence its row
 //                      row = offsets[e] + chunk_base[c][e] + rank,
-//                  then row_token / slot_row
+//                  then row_token / slot_row (and the gate of each row when asked)
 //   k_gather       per token: the bit-exact copy of the token row to each of its local
 //                  rows (read once, written k_local times, 16-byte vectors); skipped when
 //                  the caller's GEMM reads the token rows through row_token itself
@@ -181,7 +181,10 @@ __global__ __launch_bounds__(64 * RW) void k_rank(PermuteProblem p) {
     }
     if (row >= p.cap) row = -1;              // unreachable for a consistent histogram; keeps writes in bounds
     p.slot_row[t * k + j] = row;
-    if (row >= 0) p.row_token[row] = (int32_t)t;
+    if (row >= 0) {
+      p.row_token[row] = (int32_t)t;
+      if (p.row_weight) p.row_weight[row] = p.topk_w[t * k + j];
+    }
   }
 }
 

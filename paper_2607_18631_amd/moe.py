@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(HERE, "libmoe_mi355x.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
 MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER = range(4)
+MOE_FUSION_SET, MOE_FUSE_GATHER, MOE_FUSE_COMBINE = 0x10, 0x1, 0x2
 (MOE_REGION_TOPK_IDX, MOE_REGION_TOPK_W, MOE_REGION_COUNTS, MOE_REGION_OFFSETS, MOE_REGION_ROW_TOKEN,
  MOE_REGION_SLOT_ROW, MOE_REGION_X_PERM, MOE_REGION_Y_PERM, MOE_REGION_SHARED_Y) = range(9)
 
@@ -35,7 +36,7 @@ class MoEShapeC(ctypes.Structure):
                 ("F", ctypes.c_int32), ("F_shared", ctypes.c_int32), ("gate", ctypes.c_int32),
                 ("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32),
                 ("renormalize", ctypes.c_int32), ("routed_scale", ctypes.c_float),
-                ("expert_capacity", ctypes.c_int32)]
+                ("expert_capacity", ctypes.c_int32), ("fusion", ctypes.c_int32)]
 
 
 class MoEError(RuntimeError):
@@ -80,7 +81,8 @@ def lib():
 
 def shape_c(sh: MoEShape) -> MoEShapeC:
     return MoEShapeC(sh.T, sh.d, sh.E, sh.top_k, sh.e_begin, sh.E_local, sh.F, sh.F_shared, sh.gate,
-                     sh.n_group, sh.topk_group, sh.renormalize, sh.routed_scale, sh.expert_capacity)
+                     sh.n_group, sh.topk_group, sh.renormalize, sh.routed_scale, sh.expert_capacity,
+                     sh.fusion)
 
 
 def last_error() -> str:

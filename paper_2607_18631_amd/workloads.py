@@ -48,6 +48,12 @@ import numpy as np
 
 GATE_SOFTMAX = 0
 GATE_SIGMOID = 1
+# kernel structure of the layer forward (values of the C ABI's MOE_FUSION_SET / MOE_FUSE_*)
+FUSION_SET = 0x10
+FUSE_GATHER = 0x1
+FUSE_COMBINE = 0x2
+FUSION_VARIANTS = {"unfused": FUSION_SET, "gather": FUSION_SET | FUSE_GATHER,
+                   "combine": FUSION_SET | FUSE_COMBINE, "both": FUSION_SET | FUSE_GATHER | FUSE_COMBINE}
 
 # stream ids of the per-tensor generators
 _TID_X, _TID_ROUTER, _TID_W1, _TID_W3, _TID_W2 = 0, 1, 2, 3, 4
@@ -71,6 +77,7 @@ class MoEShape:
     renormalize: int = 1   # renormalise gates over the chosen experts
     routed_scale: float = 1.0
     expert_capacity: int = 0   # > 0: masked-decode layout, rows [e C, e C + C) per local expert
+    fusion: int = 0        # kernel structure of the layer forward (0 = default; see FUSION_VARIANTS)
 
     def replace(self, **kw) -> "MoEShape":
         return dataclasses.replace(self, **kw)

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(moe.EXPORTS), names
     for n in names:
         assert hasattr(L, n), n
-    assert L.moe_abi_version() == 2
+    assert L.moe_abi_version() == 3
 
 
 def test_status_strings():
@@ -38,6 +38,23 @@ def test_status_strings():
     for s in range(5):
         assert L.moe_status_string(s).decode().startswith(
             ["MOE_OK", "MOE_ERR_INVALID_ARG", "MOE_ERR_UNSUPPORTED", "MOE_ERR_WORKSPACE", "MOE_ERR_HIP"][s])
+
+
+def test_explicit_gather_fold_beyond_offset_range_is_rejected():
+    sh = BASE.replace(T=2 ** 22, d=1024, fusion=wl.FUSION_VARIANTS["gather"])
+    st, msg = _layer_call(sh)
+    assert st == moe.MOE_ERR_UNSUPPORTED and "MOE_FUSE_GATHER" in msg, (st, msg)
+    # the default structure copies the rows instead (passes validation up to the workspace)
+    st, msg = _layer_call(sh.replace(fusion=0))
+    assert st == moe.MOE_ERR_WORKSPACE, (st, msg)
+
+
+def test_fused_combine_workspace():
+    """The folded combine adds a float32 [T, d] accumulator and a gate per row."""
+    base = moe.workspace_size(BASE, moe.MOE_WS_LAYER)
+    fused = moe.workspace_size(BASE.replace(fusion=wl.FUSION_VARIANTS["both"]), moe.MOE_WS_LAYER)
+    assert fused >= base + BASE.T * BASE.d * 4 + BASE.capacity * 4
+    assert moe.workspace_size(BASE.replace(fusion=wl.FUSION_VARIANTS["gather"]), moe.MOE_WS_LAYER) == base
 
 
 def test_masked_layout_workspace():
@@ -103,6 +120,8 @@ BASE = wl.MoEShape(T=64, d=64, E=8, top_k=2, F=64, E_local=8)
     (BASE.replace(T=2 ** 30, top_k=2), moe.MOE_ERR_UNSUPPORTED, "T * top_k"),
     (BASE.replace(expert_capacity=-1), moe.MOE_ERR_INVALID_ARG, "expert_capacity (-1) < 0"),
     (BASE.replace(expert_capacity=2 ** 28), moe.MOE_ERR_UNSUPPORTED, "E_local * expert_capacity"),
+    (BASE.replace(fusion=wl.FUSE_COMBINE), moe.MOE_ERR_INVALID_ARG, "fusion (0x2)"),
+    (BASE.replace(fusion=wl.FUSION_SET | 0x4), moe.MOE_ERR_INVALID_ARG, "fusion (0x14)"),
 ])
 def test_shape_validation(sh, status, needle):
     st, msg = _layer_call(sh)
