@@ -7,3 +7,4 @@ with the HIP kernels.  Every function is pinned by the ``-m "not gpu"`` tests in
 """
 from .moe_oracle import *  # noqa: F401,F403
 from .moe_oracle import GATE_SIGMOID, GATE_SOFTMAX  # noqa: F401
+from . import moe_backward  # noqa: F401,E402
