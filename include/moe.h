@@ -73,7 +73,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 3
+#define MOE_ABI_VERSION 4
 
 /* moe_shape_t.fusion: which of the paper's four kernel structures moe_layer_forward runs
  * (Section 4, kernel generation: fuse_gather folds the token permute into the first GEMM's
@@ -104,7 +104,8 @@ typedef enum moe_ws_kind {
   MOE_WS_ROUTE = 0,
   MOE_WS_PERMUTE = 1,
   MOE_WS_FFN = 2,
-  MOE_WS_LAYER = 3
+  MOE_WS_LAYER = 3,
+  MOE_WS_FFN_BWD = 4
 } moe_ws_kind_t;
 
 /* Named regions inside a MOE_WS_LAYER workspace (moe_workspace_offset). */
@@ -204,6 +205,27 @@ int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x
 int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets,
                     const void* w13, const void* w2, void* y_perm,
                     void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the grouped SwiGLU expert MLP (the paper's training leg, Section 4, engine
+ * registration: the backward composes the expert kernels' dual GEMMs in transposed layout
+ * for the activation gradient and per-expert products for the weight gradients).
+ * For the rows r of local expert e (the segments of moe_grouped_ffn, either layout) and
+ * the gradient dy_perm of its output rows:
+ *   H = x W1^T, U = x W3^T (recomputed), dA = dy W2,
+ *   dH = dA * U * silu'(H), dU = dA * silu(H),
+ *   dx_perm[r] = [dH dU] w13                  (bf16 [cap, d]; rows outside every segment are
+ *                                              not written)
+ *   dw13[e] = [dH dU]^T x,  dw2[e] = dy^T (silu(H) * U)   (bf16 [E_local, 2F, d] / [E_local, d, F];
+ *                                              an expert without rows gets zeros)
+ * fp32 accumulation; dA, [dH dU] and the recomputed activation are rounded to bf16 once
+ * each (workspace), as are the results.  The activation-gradient GEMMs read w2 and w13 in
+ * their stored layout (the transposed operand of the forward), the weight-gradient GEMMs
+ * read the row-major activations as transposed operands (no transposed copies are made).
+ * ws: MOE_WS_FFN_BWD bytes. */
+int moe_grouped_ffn_backward(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets,
+                             const void* w13, const void* w2, const void* dy_perm,
+                             void* dx_perm, void* dw13, void* dw2,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /* Gate-weighted combine (steps 10-11):
  *   out[t] = bf16( sum over slots j with slot_row[t,j] >= 0 of topk_w[t,j] * y_perm[slot_row[t,j]]

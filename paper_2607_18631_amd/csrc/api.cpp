@@ -116,6 +116,8 @@ size_t ws_permute(const moe_shape_t* s) {
   return 2 * align_up((size_t)moe::permute_blocks(s->T) * s->E_local * sizeof(int32_t));
 }
 size_t ws_ffn(const moe_shape_t* s) { return align_up((size_t)capacity(s) * s->F * sizeof(uint16_t)); }
+// backward: dA [cap, F], [dH dU] [cap, 2F], recomputed activation [cap, F] (bf16)
+size_t ws_ffn_bwd(const moe_shape_t* s) { return 4 * ws_ffn(s); }
 
 struct LayerLayout {
   size_t region[MOE_REGION_COUNT_];
@@ -158,6 +160,7 @@ size_t ws_need(const moe_shape_t* s, int kind) {
     case MOE_WS_PERMUTE: return ws_permute(s);
     case MOE_WS_FFN: return ws_ffn(s);
     case MOE_WS_LAYER: return layer_layout(s).total;
+    case MOE_WS_FFN_BWD: return ws_ffn_bwd(s);
     default: return 0;
   }
 }
@@ -361,6 +364,97 @@ int do_combine(const moe_shape_t* s, const void* y_perm, const int32_t* slot_row
   return hip_status(moe::launch_combine(c, st), "combine launch");
 }
 
+// Expert-MLP backward (arguments validated): dA = dY W2, the up-projection recomputed with
+// the SwiGLU-backward epilogue, dX = [dH dU] w13, dW2 = dY^T A, dW13 = [dH dU]^T X.
+int do_ffn_backward(const moe_shape_t* s, const void* x_perm, const int32_t* offsets, const void* w13,
+                    const void* w2, const void* dy, void* dx, void* dw13, void* dw2, void* ws, hipStream_t st) {
+  const int64_t cap = capacity(s);
+  const int d = s->d, F = s->F, E = s->E_local, C = s->expert_capacity;
+  auto* da = at<moe::bf16_t>(ws, 0);
+  auto* act = at<moe::bf16_t>(ws, ws_ffn(s));
+  auto* dhu = at<moe::bf16_t>(ws, 2 * ws_ffn(s));
+  const int64_t rows_hint = std::max<int64_t>(1, cap / E);
+  moe::GemmBwdProblem g{};
+  g.offsets = offsets;
+  g.groups = E;
+  g.seg_stride = C;
+  g.max_rows = cap;
+  g.rows_hint = rows_hint;
+  // dA = dY W2 (W2 [d][F] read as the transposed operand)
+  g.mode = moe::BWD_ROWS;
+  g.x_mn = false;
+  g.w_mn = true;
+  g.X = static_cast<const moe::bf16_t*>(dy);
+  g.ldx = d;
+  g.W = static_cast<const moe::bf16_t*>(w2);
+  g.ldw = F;
+  g.w_group_stride = (int64_t)d * F;
+  g.N = F;
+  g.K = d;
+  g.Y = da;
+  g.ldy = F;
+  if (s->T > 0) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dA launch"));
+  // recompute H, U; dH, dU and the activation from dA
+  moe::GemmProblem up{};
+  up.X = static_cast<const moe::bf16_t*>(x_perm);
+  up.ldx = d;
+  up.offsets = offsets;
+  up.groups = E;
+  up.rows_single = cap;
+  up.max_rows = cap;
+  up.seg_stride = C;
+  up.rows_hint = rows_hint;
+  up.W = static_cast<const moe::bf16_t*>(w13);
+  up.w_group_stride = (int64_t)2 * F * d;
+  up.N = F;
+  up.K = d;
+  up.Y = dhu;
+  up.ldy = 2 * (int64_t)F;
+  up.epi = moe::EPI_SWIGLU_BWD;
+  up.dact = da;
+  up.act_out = act;
+  if (s->T > 0) CHECK(hip_status(moe::launch_grouped_gemm(up, st), "SwiGLU backward launch"));
+  // dX = [dH dU] w13 (w13 [2F][d] read as the transposed operand)
+  g.X = dhu;
+  g.ldx = 2 * F;
+  g.W = static_cast<const moe::bf16_t*>(w13);
+  g.ldw = d;
+  g.w_group_stride = (int64_t)2 * F * d;
+  g.N = d;
+  g.K = 2 * F;
+  g.Y = static_cast<moe::bf16_t*>(dx);
+  g.ldy = d;
+  if (s->T > 0) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dX launch"));
+  // weight gradients: reductions over each expert's rows (also with no tokens: then every
+  // segment is empty and the launches write zeros)
+  moe::GemmBwdProblem w = g;
+  w.mode = moe::BWD_KSEG;
+  w.x_mn = w.w_mn = true;
+  w.w_group_stride = 0;
+  // dW2[e] = dY^T A: [d, F]
+  w.X = static_cast<const moe::bf16_t*>(dy);
+  w.ldx = d;
+  w.W = act;
+  w.ldw = F;
+  w.M = d;
+  w.N = F;
+  w.Y = static_cast<moe::bf16_t*>(dw2);
+  w.ldy = F;
+  w.y_group_stride = (int64_t)d * F;
+  CHECK(hip_status(moe::launch_gemm_bwd(w, st), "dW2 launch"));
+  // dW13[e] = [dH dU]^T X: [2F, d]
+  w.X = dhu;
+  w.ldx = 2 * F;
+  w.W = static_cast<const moe::bf16_t*>(x_perm);
+  w.ldw = d;
+  w.M = 2 * F;
+  w.N = d;
+  w.Y = static_cast<moe::bf16_t*>(dw13);
+  w.ldy = d;
+  w.y_group_stride = (int64_t)2 * F * d;
+  return hip_status(moe::launch_gemm_bwd(w, st), "dW13 launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -382,7 +476,7 @@ const char* moe_last_error(void) { return g_err.c_str(); }
 
 size_t moe_workspace_size(const moe_shape_t* shape, int kind) {
   if (check_shape(shape) != MOE_OK) return 0;
-  if (kind < MOE_WS_ROUTE || kind > MOE_WS_LAYER) {
+  if (kind < MOE_WS_ROUTE || kind > MOE_WS_FFN_BWD) {
     fail(MOE_ERR_INVALID_ARG, "workspace kind (%d) unknown", kind);
     return 0;
   }
@@ -446,6 +540,27 @@ int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t*
   CHECK(check_ws(shape, MOE_WS_FFN, ws, ws_bytes));
   CHECK(do_ffn(x_perm, offsets, shape->E_local, capacity(shape), w13, w2, shape->d, shape->F, ws, y_perm,
                as_stream(stream), nullptr, 0, nullptr, Gather{}, 0, shape->expert_capacity));
+  return ok();
+}
+
+int moe_grouped_ffn_backward(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets,
+                             const void* w13, const void* w2, const void* dy_perm, void* dx_perm, void* dw13,
+                             void* dw2, void* ws, size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  if (shape->E_local > moe::kMaxGroups)
+    return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", shape->E_local, moe::kMaxGroups);
+  CHECK(check_ptr(dw13, 16, "dw13"));
+  CHECK(check_ptr(dw2, 16, "dw2"));
+  CHECK(check_ptr(offsets, 4, "offsets"));
+  CHECK(check_ws(shape, MOE_WS_FFN_BWD, ws, ws_bytes));
+  if (shape->T > 0) {
+    CHECK(check_ptr(x_perm, 16, "x_perm"));
+    CHECK(check_ptr(w13, 16, "w13"));
+    CHECK(check_ptr(w2, 16, "w2"));
+    CHECK(check_ptr(dy_perm, 16, "dy_perm"));
+    CHECK(check_ptr(dx_perm, 16, "dx_perm"));
+  }
+  CHECK(do_ffn_backward(shape, x_perm, offsets, w13, w2, dy_perm, dx_perm, dw13, dw2, ws, as_stream(stream)));
   return ok();
 }
 

@@ -46,29 +46,46 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "gemm_device.hpp"
 #include "kernels.hpp"
 
 namespace moe {
+
+// device properties, queried once per device
+struct DevInfo {
+  int cus = 0;
+  int lds = 0;
+};
+static DevInfo g_dev[64];
+
+static DevInfo& dev_info() {
+  static DevInfo fallback{256, 65536};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fallback;
+  DevInfo& d = g_dev[dev];
+  if (d.cus == 0) {
+    int n = 0, l = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || l <= 0)
+      l = 65536;
+    d.lds = l;
+    d.cus = n;
+  }
+  return d;
+}
+int cu_count() { return dev_info().cus; }
+int lds_limit() { return dev_info().lds; }
+
 namespace {
+
+// epilogues whose weight tile pairs gate rows [0, N) with up rows [N, 2N)
+constexpr bool swiglu_pairs(int epi) { return epi == EPI_SWIGLU || epi == EPI_SWIGLU_BWD; }
 
 #ifndef MOE_BAND_M
 #define MOE_BAND_M 8
 #endif
 constexpr int BAND_M = MOE_BAND_M;   // m-tiles per band of the tile order
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"I"(N) : "memory");
-}
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-__device__ __forceinline__ void raw_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// 16-byte direct-to-LDS copy of one wave instruction: lane i fetches `src` (its own
-// address) into bytes [16 i, 16 i + 16) after the wave-uniform LDS address `dst`.
-__device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
-}
 
 // Instruction-scheduler directives for one MFMA K-step: an MFMA first, then the next
 // step's LDS reads two at a time between MFMAs, then the remaining MFMAs.
@@ -91,37 +108,7 @@ __device__ __forceinline__ void sched_step() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BK>
-struct Swz {
-  static constexpr int CPR = BK / 8;            // 16-byte chunks per row
-  static constexpr int RPG = 16 / CPR;          // rows per 256-byte bank cycle
-  __device__ static __forceinline__ int f(int row) { return (row / RPG) % CPR; }
-  __device__ static __forceinline__ int off(int row, int chunk) { return row * BK + ((chunk ^ f(row)) << 3); }
-};
 
-// Block-wide exclusive scan of one int per thread (NTH threads); returns the block total.
-template <int NTH>
-__device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int inc = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int n = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += n;
-  }
-  if (lane == 63) s_tmp[wave] = inc;
-  __syncthreads();
-  int wbase = 0, total = 0;
-#pragma unroll
-  for (int w = 0; w < NTH / 64; ++w) {
-    int t = s_tmp[w];
-    if (w < wave) wbase += t;
-    total += t;
-  }
-  excl = wbase + inc - v;
-  __syncthreads();
-  return total;
-}
 
 // ---------------------------------------------------------------------------------------
 // Tile table, tile decoding, slice copies, epilogue
@@ -200,11 +187,6 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
   return ts;
 }
 
-// Workgroup b's first tile: adjacent tiles go to workgroups of one XCD (b runs on XCD b % 8).
-__device__ __forceinline__ int first_tile_slot() {
-  const int G = gridDim.x;
-  return (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
-}
 
 // One tile: token rows [row0, min(row0 + BM, row_end)) of operand X against output tile ni
 // of the weights W, results into Y.
@@ -318,7 +300,7 @@ struct CopyPlan {
     for (int j = 0; j < LW; ++j) {
       const int r = (wave + NW * j) * RPI + li_row;
       wchunk[j] = li_pc ^ Z::f(r);
-      if (EPI == EPI_SWIGLU) {
+      if (swiglu_pairs(EPI)) {
         const int half = ((wave + NW * j) * RPI) >= BN / 2;  // uniform per instruction
         const int f0 = t.ni * (BN / 2);
         const int f = min(f0 + (r - half * (BN / 2)), p.N - 1);
@@ -364,7 +346,7 @@ struct CopyPlan {
 // wave owns the gate rows and the matching up rows of its features in a SwiGLU tile).
 template <int EPI, int BN, int WGN, int FN>
 __device__ __forceinline__ int frag_wrow(int wn, int b) {
-  if (EPI == EPI_SWIGLU) {
+  if (swiglu_pairs(EPI)) {
     constexpr int HALF_W = BN / 2 / WGN;
     return (b < FN / 2) ? wn * HALF_W + b * 32 : BN / 2 + wn * HALF_W + (b - FN / 2) * 32;
   }
@@ -381,7 +363,43 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
   for (int a = 0; a < FM; ++a) {
     const int row = t.row0 + trow + a * astride + (lane & 31);
     if (row >= t.row_end) continue;
-    if (EPI == EPI_SWIGLU) {
+    if (EPI == EPI_SWIGLU_BWD) {
+      // recomputed gate h and up u: dh = dA u silu'(h), du = dA silu(h), a = silu(h) u
+      bf16_t* yrow = reinterpret_cast<bf16_t*>(t.Y) + (int64_t)row * p.ldy;
+      const bf16_t* darow = p.dact + (int64_t)row * p.N;
+      bf16_t* arow = p.act_out + (int64_t)row * p.N;
+#pragma unroll
+      for (int b = 0; b < FN / 2; ++b) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int col = fcol + b * 32 + 8 * q + 4 * (lane >> 5);
+          if (col >= p.N) continue;
+          const uint2 dav = *reinterpret_cast<const uint2*>(darow + col);
+          const float da[4] = {bf16_to_f32(dav.x & 0xffffu), bf16_to_f32(dav.x >> 16), bf16_to_f32(dav.y & 0xffffu),
+                               bf16_to_f32(dav.y >> 16)};
+          float dh[4], du[4], av[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float h = acc[a][b][4 * q + e], u = acc[a][b + FN / 2][4 * q + e];
+            const float sg = 1.0f / (1.0f + __expf(-h));
+            const float silu = h * sg;
+            av[e] = silu * u;
+            du[e] = da[e] * silu;
+            dh[e] = da[e] * u * sg * (1.0f + h * (1.0f - sg));
+          }
+          uint2 v;
+          v.x = pack_bf16x2(dh[0], dh[1]);
+          v.y = pack_bf16x2(dh[2], dh[3]);
+          *reinterpret_cast<uint2*>(yrow + col) = v;
+          v.x = pack_bf16x2(du[0], du[1]);
+          v.y = pack_bf16x2(du[2], du[3]);
+          *reinterpret_cast<uint2*>(yrow + p.N + col) = v;
+          v.x = pack_bf16x2(av[0], av[1]);
+          v.y = pack_bf16x2(av[2], av[3]);
+          *reinterpret_cast<uint2*>(arow + col) = v;
+        }
+      }
+    } else if (EPI == EPI_SWIGLU) {
       bf16_t* yrow = reinterpret_cast<bf16_t*>(t.Y) + (int64_t)row * p.ldy;
 #pragma unroll
       for (int b = 0; b < FN / 2; ++b) {
@@ -524,12 +542,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   constexpr int NW = WGM * WGN, NTH = 64 * NW;
   constexpr int WM = BM / WGM, WN = BN / WGN;             // per-wave sub-tile
   constexpr int FM = WM / 32, FN = WN / 32;               // 32x32 fragments per wave
-  constexpr int OUTN = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
+  constexpr int OUTN = (swiglu_pairs(EPI)) ? BN / 2 : BN;
   constexpr int SLICE = (BM + BN) * BK;                   // bf16 elements per ring slot
   using CP = CopyPlan<BM, BN, BK, NW, EPI>;
   constexpr int L = CP::L;
   static_assert(FM >= 1 && FN >= 1, "tile too small");
-  static_assert(EPI != EPI_SWIGLU || (FN % 2 == 0 && (BN / 2 / WGN) % 32 == 0), "SwiGLU pairs gate and up fragments");
+  static_assert(!swiglu_pairs(EPI) || (FN % 2 == 0 && (BN / 2 / WGN) % 32 == 0), "SwiGLU pairs gate and up fragments");
   static_assert(STAGES >= 2 && (STAGES - 2) * L < 64, "ring depth");
 
   extern __shared__ __align__(16) uint8_t smem[];
@@ -627,7 +645,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nl) issue_any(kb + s, s);
 
-  const int fcol = (EPI == EPI_SWIGLU ? wn * (BN / 2 / WGN) : wn * WN);
+  const int fcol = (swiglu_pairs(EPI) ? wn * (BN / 2 / WGN) : wn * WN);
   while (true) {
     f32x16 acc[FM][FN];
     zero_acc(acc);
@@ -694,29 +712,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   }
 }
 
-struct DevInfo {
-  int cus = 0;
-  int lds = 0;
-};
-DevInfo g_dev[64];
-
-DevInfo& dev_info() {
-  static DevInfo fallback{256, 65536};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fallback;
-  DevInfo& d = g_dev[dev];
-  if (d.cus == 0) {
-    int n = 0, l = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || l <= 0)
-      l = 65536;
-    d.lds = l;
-    d.cus = n;
-  }
-  return d;
-}
-int cu_count() { return dev_info().cus; }
-int lds_limit() { return dev_info().lds; }
 
 // Persistent launch of kernel `fn` (nth threads, lds bytes of dynamic LDS): grid = the
 // smaller of an upper bound of the launch's tile count and the resident workgroups, rounded
@@ -754,7 +749,7 @@ hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
   static int per_cu = 0;
   const void* fn = reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>);
   return launch_persistent(fn, per_cu, 64 * WGM * WGN, (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t), BM,
-                           EPI == EPI_SWIGLU ? BN / 2 : BN, p, stream);
+                           swiglu_pairs(EPI) ? BN / 2 : BN, p, stream);
 }
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI>
@@ -861,6 +856,13 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
 #endif
   switch (p.epi) {
     case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
+    case EPI_SWIGLU_BWD:
+      if (!p.dact || !p.act_out || p.rows2 > 0 || p.ldy != 2 * (int64_t)p.N) return hipErrorInvalidValue;
+      switch (tier) {      // the tiers of the forward up-projection (same operand shapes)
+        case 20: return launch_tile<64, 128, 64, 3, 2, 2, EPI_SWIGLU_BWD>(p, stream);
+        case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI_SWIGLU_BWD>(p, stream);
+        default: return launch_tile<256, 256, 64, 2, 4, 2, EPI_SWIGLU_BWD>(p, stream);
+      }
     case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
     case EPI_SCATTER:
       if (p.scatter_rows < 1) return hipErrorInvalidValue;

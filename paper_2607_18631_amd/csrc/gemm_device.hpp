@@ -1,0 +1,61 @@
+// Device helpers shared by the grouped GEMMs (forward and backward): slice copies straight
+// into LDS, wait / barrier primitives, the K-major LDS swizzle, a block-wide scan and the
+// XCD-aware first tile of a persistent workgroup.
+#pragma once
+#include "common.hpp"
+
+namespace moe {
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"I"(N) : "memory");
+}
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ void raw_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// 16-byte direct-to-LDS copy of one wave instruction: lane i fetches `src` (its own
+// address) into bytes [16 i, 16 i + 16) after the wave-uniform LDS address `dst`.
+__device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+template <int BK>
+struct Swz {
+  static constexpr int CPR = BK / 8;            // 16-byte chunks per row
+  static constexpr int RPG = 16 / CPR;          // rows per 256-byte bank cycle
+  __device__ static __forceinline__ int f(int row) { return (row / RPG) % CPR; }
+  __device__ static __forceinline__ int off(int row, int chunk) { return row * BK + ((chunk ^ f(row)) << 3); }
+};
+
+// Block-wide exclusive scan of one int per thread (NTH threads); returns the block total.
+template <int NTH>
+__device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int n = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += n;
+  }
+  if (lane == 63) s_tmp[wave] = inc;
+  __syncthreads();
+  int wbase = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < NTH / 64; ++w) {
+    int t = s_tmp[w];
+    if (w < wave) wbase += t;
+    total += t;
+  }
+  excl = wbase + inc - v;
+  __syncthreads();
+  return total;
+}
+
+// Workgroup b's first tile: adjacent tiles go to workgroups of one XCD (b runs on XCD b % 8).
+__device__ __forceinline__ int first_tile_slot() {
+  const int G = gridDim.x;
+  return (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+}
+
+}  // namespace moe

@@ -9,12 +9,16 @@ typedef uint16_t bf16_t;
 
 constexpr int kMaxGroups = 1024;  // E_local limit of the grouped GEMM's in-LDS tile table
 
-enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2, EPI_SCATTER = 3 };
+enum Epilogue { EPI_BF16 = 0, EPI_SWIGLU = 1, EPI_F32 = 2, EPI_SCATTER = 3, EPI_SWIGLU_BWD = 4 };
 
 // One grouped GEMM  Y[r, n] = sum_k X[r, k] * W_g[n, k]  for every group g and every
 // row r in [offsets[g], offsets[g+1]).  Both operands are K-contiguous.
 // EPI_SWIGLU: W_g holds 2N rows (gate rows [0,N), up rows [N,2N)) and
 //             Y[r, n] = bf16(silu(gate) * up).
+// EPI_SWIGLU_BWD: the up-projection recomputed in the backward; with gate h and up u of row r,
+//             feature n, and dA = dact[r, n]:  Y[r, n] = bf16(dA * u * silu'(h)),
+//             Y[r, N + n] = bf16(dA * silu(h)) (row stride ldy = 2N), and act_out[r, n] =
+//             bf16(silu(h) * u) (row stride N), the activation the weight gradient of W2 needs.
 // EPI_SCATTER: float32 Y rows are token rows: Y[tok(r), n] += w(r) * (X W_g^T)[r, n] by
 //             atomics, tok(r) = scatter_token[r] and w(r) = scatter_weight[r] for the grouped
 //             rows (identity and 1 when the pointers are null, and for the extra group).
@@ -57,9 +61,49 @@ struct GemmProblem {
   const int32_t* scatter_token;
   const float* scatter_weight;
   int64_t scatter_rows;
+  // EPI_SWIGLU_BWD: gradient of the activation [rows, N] and the recomputed activation
+  const bf16_t* dact;
+  bf16_t* act_out;
 };
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
+
+// compute units and the LDS bytes per workgroup of the current device (queried once)
+int cu_count();
+int lds_limit();
+
+// Grouped GEMMs of the expert-MLP backward:  Y[m, n] = sum_k X[m, k] * W[n, k]  with each
+// operand either K-major (element (r, k) at base + r * ld + k) or MN-major (element (k, r) at
+// base + k * ld + r, the transposed layout of a row-major activation or weight).
+//  mode BWD_ROWS: group g owns rows [seg_begin(g), seg_end(g)) of X and Y (as the forward),
+//                 K = p.K, weights W + g * w_group_stride;
+//  mode BWD_KSEG: group g reduces over the rows [seg_begin(g), seg_end(g)) of two row-major
+//                 activations (X and W both MN-major, k = row): Y_g = Y + g * y_group_stride,
+//                 an M x N matrix per group (weight gradients; an empty group writes zeros).
+// Segments: monotone offsets[groups + 1], or seg_stride > 0 with offsets = counts[groups]
+// (group g owns [g * seg_stride, g * seg_stride + min(count, seg_stride))).
+enum BwdMode { BWD_ROWS = 0, BWD_KSEG = 1 };
+struct GemmBwdProblem {
+  int32_t mode;
+  bool x_mn, w_mn;            // operand layouts (MN-major when set)
+  const bf16_t* X;
+  int64_t ldx;
+  const bf16_t* W;
+  int64_t ldw;
+  int64_t w_group_stride;     // BWD_ROWS
+  const int32_t* offsets;
+  int32_t groups;
+  int32_t seg_stride;
+  int64_t max_rows;           // host-known bound of the rows (grid sizing, offsets clamp)
+  int64_t rows_hint;          // expected rows per group (BWD_ROWS tile shape), 0 = unknown
+  int32_t M;                  // BWD_KSEG: output rows per group
+  int32_t N;                  // output columns
+  int32_t K;                  // BWD_ROWS: reduction length
+  bf16_t* Y;
+  int64_t ldy;
+  int64_t y_group_stride;     // BWD_KSEG
+};
+hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream);
 
 // Number of K chunks the router-logits GEMM (T x E outputs, K = d) runs in: enough (m, n, k)
 // tiles for one per compute unit of the chip, every chunk non-empty.  Depends on the shape

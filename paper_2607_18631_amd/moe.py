@@ -18,14 +18,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmoe_mi355x.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
-MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER = range(4)
+MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER, MOE_WS_FFN_BWD = range(5)
 MOE_FUSION_SET, MOE_FUSE_GATHER, MOE_FUSE_COMBINE = 0x10, 0x1, 0x2
 (MOE_REGION_TOPK_IDX, MOE_REGION_TOPK_W, MOE_REGION_COUNTS, MOE_REGION_OFFSETS, MOE_REGION_ROW_TOKEN,
  MOE_REGION_SLOT_ROW, MOE_REGION_X_PERM, MOE_REGION_Y_PERM, MOE_REGION_SHARED_Y) = range(9)
 
 EXPORTS = ["moe_abi_version", "moe_status_string", "moe_last_error", "moe_workspace_size",
            "moe_workspace_offset", "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
-           "moe_layer_forward", "moe_layer_forward_traced"]
+           "moe_layer_forward", "moe_layer_forward_traced", "moe_grouped_ffn_backward"]
 MOE_STEP_NAMES = ["router_gemm", "gate", "histogram", "permute", "ffn_up", "ffn_down", "shared_up",
                   "shared_down", "combine"]
 
@@ -69,11 +69,13 @@ def lib():
         L.moe_permute.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_grouped_ffn.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_combine.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp]
+        L.moe_grouped_ffn_backward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                               _vp]
         L.moe_layer_forward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_layer_forward_traced.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                                ctypes.POINTER(_vp), _vp]
         for f in ("moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine", "moe_layer_forward",
-                  "moe_layer_forward_traced"):
+                  "moe_layer_forward_traced", "moe_grouped_ffn_backward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -139,6 +141,12 @@ def moe_permute(sh, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, w
 def moe_grouped_ffn(sh, x_perm, offsets, w13, w2, y_perm, ws=None, stream=None):
     _check(lib().moe_grouped_ffn(ctypes.byref(shape_c(sh)), _p(x_perm), _p(offsets), _p(w13), _p(w2), _p(y_perm),
                                  _p(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def moe_grouped_ffn_backward(sh, x_perm, offsets, w13, w2, dy_perm, dx_perm, dw13, dw2, ws=None, stream=None):
+    _check(lib().moe_grouped_ffn_backward(ctypes.byref(shape_c(sh)), _p(x_perm), _p(offsets), _p(w13), _p(w2),
+                                          _p(dy_perm), _p(dx_perm), _p(dw13), _p(dw2), _p(ws),
+                                          0 if ws is None else ws.numel(), _stream(stream)))
 
 
 def moe_combine(sh, y_perm, slot_row, topk_w, shared_y, out, stream=None):

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(moe.EXPORTS), names
     for n in names:
         assert hasattr(L, n), n
-    assert L.moe_abi_version() == 3
+    assert L.moe_abi_version() == 4
 
 
 def test_status_strings():
@@ -72,7 +72,7 @@ def test_masked_layout_workspace():
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))
 def test_workspace_sizes(name):
     sh = wl.WORKLOADS[name].shape
-    for kind in range(4):
+    for kind in range(5):
         n = moe.workspace_size(sh, kind)
         assert n > 0 and n % 256 == 0
     layer = moe.workspace_size(sh, moe.MOE_WS_LAYER)
