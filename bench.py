@@ -246,6 +246,48 @@ def fusion_matrix_run(workload, steps):
     return sh0, rows
 
 
+def backward_run(workload, steps):
+    """The expert-MLP backward (moe_grouped_ffn_backward) on the expert-ordered rows of one
+    routed batch of the workload (its forward run unfused, so x_perm is materialised), next to
+    the forward expert MLP (moe_grouped_ffn) on the same rows.  Per-call times: warmup 10,
+    median of 3 round medians of `steps` calls."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    inputs = wl.make_inputs(workload)
+    sh = inputs["shape"].replace(fusion=wl.FUSION_VARIANTS["unfused"])
+    layer = moe.DeviceLayer(dict(inputs, shape=sh), device="cuda:0")
+    layer.forward()
+    torch.cuda.synchronize()
+    cap, d, F, E = sh.capacity, sh.d, sh.F, sh.E_local
+    x_perm = layer.region(moe.MOE_REGION_X_PERM, torch.bfloat16, (cap, d))
+    offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (E + 1,))
+    n_loc = int(offsets[-1].item())
+    g = torch.Generator(device="cuda:0").manual_seed(5)
+    dy = torch.randn((cap, d), generator=g, device="cuda:0").to(torch.bfloat16)
+    dx = torch.empty((cap, d), dtype=torch.bfloat16, device="cuda:0")
+    dw13 = torch.empty((E, 2 * F, d), dtype=torch.bfloat16, device="cuda:0")
+    dw2 = torch.empty((E, d, F), dtype=torch.bfloat16, device="cuda:0")
+    ws = moe.alloc_workspace(sh, moe.MOE_WS_FFN_BWD, "cuda:0")
+    y = torch.empty((cap, d), dtype=torch.bfloat16, device="cuda:0")
+    ws_f = moe.alloc_workspace(sh, moe.MOE_WS_FFN, "cuda:0")
+    t_bwd = timed_median(lambda: moe.moe_grouped_ffn_backward(sh, x_perm, offsets, layer.w13, layer.w2, dy, dx,
+                                                              dw13, dw2, ws), steps)
+    t_fwd = timed_median(lambda: moe.moe_grouped_ffn(sh, x_perm, offsets, layer.w13, layer.w2, y, ws_f), steps)
+    assert bool(torch.isfinite(dw13.float()).all()) and bool(torch.isfinite(dx[:n_loc].float()).all())
+    unit = d * F * n_loc
+    log(f"backward {t_bwd * 1e3:.1f} us, forward {t_fwd * 1e3:.1f} us on {n_loc} rows")
+    return sh, {"local_rows": n_loc, "backward_us": t_bwd * 1e3, "forward_us": t_fwd * 1e3,
+                # executed MFMA work: dA 2, recomputed up-projection 4, dX 4, dW2 2, dW13 4 (x d F rows)
+                "backward_tflops_executed": 16.0 * unit / (t_bwd * 1e-3) / 1e12,
+                # the gradient products alone (twice the forward's 6 d F rows)
+                "backward_tflops_gradients": 12.0 * unit / (t_bwd * 1e-3) / 1e12,
+                "forward_tflops": 6.0 * unit / (t_fwd * 1e-3) / 1e12,
+                "backward_frac_of_bf16_peak": 16.0 * unit / (t_bwd * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -286,6 +328,8 @@ def main():
                          "layout, eager and replayed from a HIP graph, instead of the layer benchmark")
     ap.add_argument("--fusion-matrix", action="store_true",
                     help="time the layer of --workload in the four fuse_gather x fuse_combine structures")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the expert-MLP backward on one routed batch of --workload")
     ap.add_argument("--capacity", type=int, default=0,
                     help="expert capacity of --masked-decode (0: T, every slot kept)")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
@@ -327,6 +371,16 @@ def main():
                                       "the capturing stream",
                           "masked_equals_offsets_output": same,
                           "rows": rows}), flush=True)
+        return
+    if args.backward:
+        sh, row = backward_run(args.workload, max(args.steps, 10))
+        print(json.dumps({"metric": "expert-MLP backward (dX, dW13, dW2) latency and TFLOP/s, 1 MI355X",
+                          "unit": "us", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "config": {"workload": args.workload, "T": sh.T, "d": sh.d, "E": sh.E, "top_k": sh.top_k,
+                                     "E_local": sh.E_local, "F": sh.F},
+                          "protocol": "warmup 10; median of 3 round medians of the per-call event times",
+                          **row}), flush=True)
         return
     if args.fusion_matrix:
         sh0, rows = fusion_matrix_run(args.workload, max(args.steps, 10))

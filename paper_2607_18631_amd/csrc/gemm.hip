@@ -87,26 +87,6 @@ constexpr bool swiglu_pairs(int epi) { return epi == EPI_SWIGLU || epi == EPI_SW
 constexpr int BAND_M = MOE_BAND_M;   // m-tiles per band of the tile order
 
 
-// Instruction-scheduler directives for one MFMA K-step: an MFMA first, then the next
-// step's LDS reads two at a time between MFMAs, then the remaining MFMAs.
-template <int REM>
-__device__ __forceinline__ void sched_read_pairs() {
-  if constexpr (REM > 0) {
-    __builtin_amdgcn_sched_group_barrier(0x100, REM >= 2 ? 2 : 1, 0);   // DS read(s)
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA
-    sched_read_pairs<REM - 2>();
-  }
-}
-template <int NR, int NMF>
-__device__ __forceinline__ void sched_step() {
-  if constexpr (NMF >= (NR + 1) / 2 + 1) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    sched_read_pairs<NR>();
-    if constexpr (NMF - (NR + 1) / 2 - 1 > 0)
-      __builtin_amdgcn_sched_group_barrier(0x008, NMF - (NR + 1) / 2 - 1, 0);
-  }
-  __builtin_amdgcn_sched_barrier(0);
-}
 
 
 
@@ -509,16 +489,6 @@ __device__ __forceinline__ void scatter_tile(const GemmProblem& p, const f32x16 
   }
 }
 
-// f(std::integral_constant<int, k>) with k = min(n, N) (n >= 0)
-template <int N, class F>
-__device__ __forceinline__ void with_count(int n, F&& f) {
-  if constexpr (N == 0) {
-    f(std::integral_constant<int, 0>{});
-  } else {
-    if (n >= N) f(std::integral_constant<int, N>{});
-    else with_count<N - 1>(n, f);
-  }
-}
 
 template <int FM, int FN>
 __device__ __forceinline__ void zero_acc(f32x16 (&acc)[FM][FN]) {

@@ -70,7 +70,6 @@ struct OpCopy {
   const char* base;        // element (0, 0) of the tile's K range
   int64_t ld2;             // row stride in bytes
   uint32_t off[L];         // per lane: byte offset inside a slice
-  int krow[L];             // MN: the lane's k-row inside the slice;  K-major: its chunk's first k
 
   // rlast: last valid tile row (K-major) / last valid 8-column chunk start (MN-major)
   __device__ __forceinline__ void setup(const bf16_t* b, int64_t ld, int rlast, int wave, int lane) {
@@ -82,18 +81,26 @@ struct OpCopy {
       const int row = cid / CPR, pc = cid % CPR;
       if constexpr (MN) {
         const int lc = pc ^ ((row & 3) << 2);
-        krow[j] = row;
         off[j] = (uint32_t)(row * ld2 + min(lc * 8, rlast) * 2);
       } else {
         const int lc = pc ^ Z::f(row);
-        krow[j] = lc * 8;
         off[j] = (uint32_t)(min(row, rlast) * ld2 + lc * 16);
       }
     }
   }
 
+  // k offset inside the slice of the lane's chunk in instruction j: its k-row (MN-major) or
+  // the first k of its chunk (K-major); recomputed for the tail slice only
+  __device__ __forceinline__ static int chunk_k(int j, int wave, int lane) {
+    const int cid = (wave + NW * j) * 64 + lane;
+    const int row = cid / CPR, pc = cid % CPR;
+    if constexpr (MN) return row;
+    else return (pc ^ Z::f(row)) * 8;
+  }
+
   // slice kt of a K range of klen into the LDS block dst (this wave's L instructions)
   __device__ __forceinline__ void issue(bf16_t* dst, int kt, int klen, int wave) const {
+    const int lane = threadIdx.x & 63;
     const int k0 = kt * BK;
     const bool tail = k0 + BK > klen;
     const char* sb = MN ? base + (int64_t)k0 * ld2 : base + k0 * 2;
@@ -101,8 +108,9 @@ struct OpCopy {
     for (int j = 0; j < L; ++j) {
       uint32_t o = off[j];
       if (tail) {
-        if constexpr (MN) o -= (uint32_t)(max(k0 + krow[j] - (klen - 1), 0) * ld2);
-        else o -= (uint32_t)(max(k0 + krow[j] - (klen - 8), 0) * 2);
+        const int kr = chunk_k(j, wave, lane);
+        if constexpr (MN) o -= (uint32_t)(max(k0 + kr - (klen - 1), 0) * ld2);
+        else o -= (uint32_t)(max(k0 + kr - (klen - 8), 0) * 2);
       }
       dma16(reinterpret_cast<const bf16_t*>(sb + o), dst + (wave + NW * j) * 512);
     }
@@ -121,23 +129,26 @@ struct OpCopy {
   }
 };
 
-template <int BM, int BN, int BK, int WGM, int WGN, bool XMN, bool WMN, int MODE>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p) {
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem p) {
   constexpr int NW = WGM * WGN, NTH = 64 * NW;
+  static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
   constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
   constexpr int KS = BK / 16;
   constexpr int SLICE = (BM + BN) * BK;
   static_assert(FM >= 1 && FN >= 1, "wave tile");
   static_assert(MODE == BWD_KSEG || !XMN, "row segments take a K-major X");
+  static_assert(NW * 32 * WN <= SLICE, "epilogue staging fits one ring slot");
+  static_assert((32 * (WN / 8)) % 64 == 0, "epilogue pieces per wave");
   using CX = OpCopy<BM, BK, NW, XMN>;
   using CW = OpCopy<BN, BK, NW, WMN>;
   using Z = Swz<BK>;
 
   extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* ring = reinterpret_cast<bf16_t*>(smem);        // [2][X block | W block]
+  bf16_t* ring = reinterpret_cast<bf16_t*>(smem);        // [STAGES][X block | W block]
   __shared__ int s_off[kMaxGroups];                      // first row of each group
   __shared__ int s_len[kMaxGroups];                      // rows of each group
-  __shared__ int s_tp[kMaxGroups + 1];                   // row segments: first tile of each group
+  __shared__ int s_tp[MODE == BWD_ROWS ? kMaxGroups + 1 : 1];   // row segments: first tile of each group
   __shared__ int s_tmp[NW];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -244,8 +255,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
       const int blk = a * WGM + wm;                       // 32-row block of the tile
       if constexpr (XMN) {
         const int lc = blk * 4 + 2 * g1 + (q >> 1);
-#pragma unroll
-        for (int h = 0; h < 2; ++h) xo[a][h] = (8 * hi + 4 * h + j) * BM + ((lc ^ (j << 2)) << 3) + (q & 1) * 4;
+        xo[a][0] = (8 * hi + j) * BM + ((lc ^ (j << 2)) << 3) + (q & 1) * 4;   // h = 1: + 4 BM
+        xo[a][1] = 0;
       } else {
         const int r = blk * 32 + (lane & 31);
         xo[a][0] = r * BK;
@@ -257,8 +268,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
       const int blk = wn * FN + b;
       if constexpr (WMN) {
         const int lc = blk * 4 + 2 * g1 + (q >> 1);
-#pragma unroll
-        for (int h = 0; h < 2; ++h) wo[b][h] = (8 * hi + 4 * h + j) * BN + ((lc ^ (j << 2)) << 3) + (q & 1) * 4;
+        wo[b][0] = (8 * hi + j) * BN + ((lc ^ (j << 2)) << 3) + (q & 1) * 4;   // h = 1: + 4 BN
+        wo[b][1] = 0;
       } else {
         const int r = blk * 32 + (lane & 31);
         wo[b][0] = r * BK;
@@ -268,11 +279,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
   }
   const int hi = lane >> 5;
   auto frag_x = [&](const bf16_t* blk, int a, int ks) -> bf16x8 {
-    if constexpr (XMN) return tr_pair(blk + ks * 16 * BM + xo[a][0], blk + ks * 16 * BM + xo[a][1]);
+    if constexpr (XMN) return tr_pair(blk + ks * 16 * BM + xo[a][0], blk + ks * 16 * BM + 4 * BM + xo[a][0]);
     else return *reinterpret_cast<const bf16x8*>(blk + xo[a][0] + (((ks * 2 + hi) ^ xo[a][1]) << 3));
   };
   auto frag_w = [&](const bf16_t* blk, int b, int ks) -> bf16x8 {
-    if constexpr (WMN) return tr_pair(blk + ks * 16 * BN + wo[b][0], blk + ks * 16 * BN + wo[b][1]);
+    if constexpr (WMN) return tr_pair(blk + ks * 16 * BN + wo[b][0], blk + ks * 16 * BN + 4 * BN + wo[b][0]);
     else return *reinterpret_cast<const bf16x8*>(blk + wo[b][0] + (((ks * 2 + hi) ^ wo[b][1]) << 3));
   };
 
@@ -282,7 +293,40 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
   BTile td = decode(tile);
   setup(td);
   int nl = (td.klen + BK - 1) / BK;
-  if (nl > 0) issue(0, 0, td.klen);
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nl) issue(s, s, td.klen);
+
+  // sync_slice(i): slice i landed for every wave and every wave is done reading slice i - 1's
+  // slot, which then takes slice i + STAGES - 1 (a partial last slice is zeroed past the K
+  // range).  Slices issued after slice i may stay in flight, except on a tile's first slice:
+  // the previous tile's result stores are queued behind its copies then, and loads and stores
+  // are not assumed to complete in order, so everything is drained.
+  constexpr int L = CX::L + CW::L;                       // copy instructions per slice and wave
+  auto sync_slice = [&](int i) {
+    const int after = min(STAGES - 2, nl - 1 - i);
+    if (STAGES >= 4 && i > 0 && after >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * L : 0)>();
+    else if (STAGES >= 3 && i > 0 && after >= 1) wait_vmcnt<(STAGES >= 3 ? L : 0)>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (i + STAGES - 1 < nl) issue(i + STAGES - 1, (i + STAGES - 1) % STAGES, td.klen);
+    if (i < nl && (i + 1) * BK > td.klen) {
+      bf16_t* xs = ring + (i % STAGES) * SLICE;
+      CX::zero_tail(xs, i, td.klen, tid, NTH);
+      CW::zero_tail(xs + BM * BK, i, td.klen, tid, NTH);
+      lds_barrier();
+    }
+  };
+  constexpr int NR = FM * (XMN ? 2 : 1) + FN * (WMN ? 2 : 1);   // LDS reads per K-step
+  bf16x8 fx[2][FM], fw[2][FN];
+  int na_cur = FM;                                       // live token fragments of the current tile
+  auto load_frags = [&](int buf, const bf16_t* xs, int ks) {
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+      if (a < na_cur) fx[buf][a] = frag_x(xs, a, ks);
+#pragma unroll
+    for (int b = 0; b < FN; ++b) fw[buf][b] = frag_w(xs + BM * BK, b, ks);
+  };
 
   while (true) {
     f32x16 acc[FM][FN];
@@ -293,31 +337,43 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-    for (int i = 0; i < nl; ++i) {
-      // slice i landed everywhere, and every wave is done with slice i - 1's slot
-      wait_vmcnt<0>();
-      lds_barrier();
-      if (i + 1 < nl) issue(i + 1, (i + 1) & 1, td.klen);
-      bf16_t* xs = ring + (i & 1) * SLICE;
-      if ((i + 1) * BK > td.klen) {
-        CX::zero_tail(xs, i, td.klen, tid, NTH);
-        CW::zero_tail(xs + BM * BK, i, td.klen, tid, NTH);
-        lds_barrier();
+    // the K loop with NA live token blocks for this wave: the tile's 32-row blocks alternate over
+    // the waves (block a * WGM + wm), and blocks past the segment's end (the ragged last m-tile
+    // of a group) cost no MFMA; every wave still copies and meets every barrier
+    auto k_loop = [&](auto na) {
+      constexpr int NA = decltype(na)::value;
+      if (nl == 0) return;
+      sync_slice(0);
+      if constexpr (NA > 0) load_frags(0, ring, 0);
+      for (int i = 0; i < nl; ++i) {
+        const bf16_t* xs = ring + (i % STAGES) * SLICE;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int cur = ks & 1;
+          if (ks + 1 < KS) {
+            if constexpr (NA > 0) load_frags(cur ^ 1, xs, ks + 1);
+          } else {
+            // this step's operands are in registers: publish the next slice now, so the barrier
+            // and its first reads overlap this step's MFMAs (after the last slice the reads hit
+            // a stale slot, harmlessly)
+            sync_slice(i + 1);
+            if constexpr (NA > 0) load_frags(cur ^ 1, ring + ((i + 1) % STAGES) * SLICE, 0);
+          }
+          if constexpr (NA > 0) {
+#pragma unroll
+            for (int a = 0; a < NA; ++a)
+#pragma unroll
+              for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+            sched_step<NR, NA * FN>();
+          }
+        }
       }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 fx[FM], fw[FN];
-#pragma unroll
-        for (int a = 0; a < FM; ++a) fx[a] = frag_x(xs, a, ks);
-#pragma unroll
-        for (int b = 0; b < FN; ++b) fw[b] = frag_w(xs + BM * BK, b, ks);
-#pragma unroll
-        for (int a = 0; a < FM; ++a)
-#pragma unroll
-          for (int b = 0; b < FN; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[b], fx[a], acc[a][b], 0, 0, 0);
-      }
-    }
+    };
+    const int live_blocks = min(BM / 32, (td.m_end - td.m0 + 31) / 32);
+    const int na = __builtin_amdgcn_readfirstlane(max(0, (live_blocks - wm + WGM - 1) / WGM));
+    na_cur = na;
+    with_count<FM>(na, k_loop);
 
     // next tile's first slice goes into slot 0 once every wave is done reading the ring
     const BTile cur = td;
@@ -329,39 +385,57 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_gemm_bwd(GemmBwdProblem p
       td = decode(tile);
       setup(td);
       nl = (td.klen + BK - 1) / BK;
-      if (nl > 0) issue(0, 0, td.klen);
+#pragma unroll
+      for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nl) issue(s, s, td.klen);
     }
 
-    // epilogue: lane holds output row m0 + 32 blk + (lane & 31), columns n0 + 32 bb + 8 q + 4 hi + 0..3
+    // epilogue, one 32-row block at a time through this wave's area of the idle last ring slot:
+    // the lane's 4-column pieces (row lane & 31, columns 32 b + 8 q + 4 hi) go to LDS, then
+    // every lane stores 16-byte pieces of whole rows (WN columns each), so a store instruction
+    // writes full cache lines of 64 / (WN / 8) rows.  The 16-byte piece c of staged row r sits
+    // at piece c ^ (r % (WN / 8)), spreading the 32 rows a write instruction touches over the
+    // banks.
     bf16_t* yg = p.Y + (MODE == BWD_KSEG ? (int64_t)cur.g * p.y_group_stride : 0);
+    bf16_t* st_area = ring + (STAGES - 1) * SLICE + wave * 32 * WN;
+    constexpr int CPRW = WN / 8;                          // 16-byte pieces per staged row
 #pragma unroll
     for (int a = 0; a < FM; ++a) {
-      const int row = cur.m0 + (a * WGM + wm) * 32 + (lane & 31);
-      if (row >= cur.m_end) continue;
-      bf16_t* yrow = yg + (int64_t)row * p.ldy;
+      const int rbase = cur.m0 + (a * WGM + wm) * 32;
+      if (rbase >= cur.m_end) continue;                   // wave-uniform
 #pragma unroll
-      for (int b = 0; b < FN; ++b) {
+      for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int col = cur.n0 + (wn * FN + b) * 32 + 8 * q + 4 * hi;
-          if (col >= p.N) continue;
           uint2 v;
           v.x = pack_bf16x2(acc[a][b][4 * q + 0], acc[a][b][4 * q + 1]);
           v.y = pack_bf16x2(acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]);
-          *reinterpret_cast<uint2*>(yrow + col) = v;
+          const int r = lane & 31;
+          *reinterpret_cast<uint2*>(st_area + r * WN + (((b * 4 + q) ^ (r % CPRW)) << 3) + 4 * hi) = v;
         }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int it = 0; it < 32 * CPRW / 64; ++it) {
+        const int idx = it * 64 + lane;
+        const int r = idx / CPRW, c = idx % CPRW;
+        const int row = rbase + r, col = cur.n0 + wn * WN + c * 8;
+        const u32x4 v = ld16(st_area + r * WN + ((c ^ (r % CPRW)) << 3));
+        if (row < cur.m_end && col < p.N) st16(yg + (int64_t)row * p.ldy + col, v);
       }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
     }
     if (!more) break;
   }
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, bool XMN, bool WMN, int MODE>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC = 1>
 hipError_t launch_bwd(const GemmBwdProblem& p, hipStream_t stream) {
   static int per_cu = 0;
-  const void* fn = reinterpret_cast<const void*>(&k_gemm_bwd<BM, BN, BK, WGM, WGN, XMN, WMN, MODE>);
-  const size_t lds = (size_t)2 * (BM + BN) * BK * sizeof(bf16_t);
-  const size_t lds_static = 3 * (kMaxGroups + 1) * sizeof(int) + 64;
+  const void* fn = reinterpret_cast<const void*>(&k_gemm_bwd<BM, BN, BK, STAGES, WGM, WGN, XMN, WMN, MODE, OCC>);
+  const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t);
+  const size_t lds_static = (MODE == BWD_ROWS ? 3 : 2) * (kMaxGroups + 1) * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
   if (per_cu == 0) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -393,13 +467,25 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
   if (p.mode == BWD_ROWS) {
     // dA / dX: K-major activation rows against an MN-major weight
     if (p.x_mn || !p.w_mn || p.K < 8 || p.K % 8) return hipErrorInvalidValue;
-    if (p.rows_hint > 0 && p.rows_hint <= 128) return launch_bwd<64, 128, 64, 2, 2, false, true, BWD_ROWS>(p, stream);
-    return launch_bwd<256, 256, 64, 4, 2, false, true, BWD_ROWS>(p, stream);
+    if (p.rows_hint > 0 && p.rows_hint <= 128)
+      return launch_bwd<64, 128, 64, 3, 2, 2, false, true, BWD_ROWS>(p, stream);
+    return launch_bwd<256, 256, 64, 2, 4, 2, false, true, BWD_ROWS>(p, stream);
   }
   if (p.mode == BWD_KSEG) {
     // weight gradients: both operands row-major activations reduced over the group's rows
     if (!p.x_mn || !p.w_mn || p.M < 8 || p.M % 8) return hipErrorInvalidValue;
-    return launch_bwd<256, 256, 64, 4, 2, true, true, BWD_KSEG>(p, stream);
+    // 256 x 256 tiles, two 64-wide slices in flight: measured against 128 x 128 tiles with two
+    // or three workgroups per CU and three 32-wide slices in flight (3-10% slower at DeepSeek-V3
+    // and Mixtral shapes)
+#ifndef MOE_BWD_KSEG_CFG
+#define MOE_BWD_KSEG_CFG 0
+#endif
+    switch (MOE_BWD_KSEG_CFG) {
+      case 1: return launch_bwd<128, 128, 64, 2, 2, 2, true, true, BWD_KSEG, 2>(p, stream);
+      case 3: return launch_bwd<128, 128, 32, 4, 2, 2, true, true, BWD_KSEG, 2>(p, stream);
+      case 4: return launch_bwd<128, 128, 32, 3, 2, 2, true, true, BWD_KSEG, 3>(p, stream);
+      default: return launch_bwd<256, 256, 64, 2, 4, 2, true, true, BWD_KSEG, 1>(p, stream);
+    }
   }
   return hipErrorInvalidValue;
 }

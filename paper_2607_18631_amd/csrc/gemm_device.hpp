@@ -2,6 +2,8 @@
 // into LDS, wait / barrier primitives, the K-major LDS swizzle, a block-wide scan and the
 // XCD-aware first tile of a persistent workgroup.
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace moe {
@@ -56,6 +58,38 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int& excl) {
 __device__ __forceinline__ int first_tile_slot() {
   const int G = gridDim.x;
   return (G % 8 == 0) ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+}
+
+// Instruction-scheduler directives for one MFMA K-step: an MFMA first, then the next
+// step's LDS reads two at a time between MFMAs, then the remaining MFMAs.
+template <int REM>
+__device__ __forceinline__ void sched_read_pairs() {
+  if constexpr (REM > 0) {
+    __builtin_amdgcn_sched_group_barrier(0x100, REM >= 2 ? 2 : 1, 0);   // DS read(s)
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA
+    sched_read_pairs<REM - 2>();
+  }
+}
+template <int NR, int NMF>
+__device__ __forceinline__ void sched_step() {
+  if constexpr (NMF >= (NR + 1) / 2 + 1) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    sched_read_pairs<NR>();
+    if constexpr (NMF - (NR + 1) / 2 - 1 > 0)
+      __builtin_amdgcn_sched_group_barrier(0x008, NMF - (NR + 1) / 2 - 1, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// f(std::integral_constant<int, k>) with k = min(n, N) (n >= 0)
+template <int N, class F>
+__device__ __forceinline__ void with_count(int n, F&& f) {
+  if constexpr (N == 0) {
+    f(std::integral_constant<int, 0>{});
+  } else {
+    if (n >= N) f(std::integral_constant<int, N>{});
+    else with_count<N - 1>(n, f);
+  }
 }
 
 }  // namespace moe
