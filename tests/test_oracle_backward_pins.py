@@ -105,3 +105,103 @@ def test_grouped_backward_segments(capacity):
         np.testing.assert_array_equal(dw13[e], g13)
         np.testing.assert_array_equal(dw2[e], g2)
     assert not dx[~covered].any()
+
+
+# ---------------------------------------------------------------------------------------
+# the whole layer: an independent float64 torch implementation of the forward, differentiated
+# by torch.autograd with the oracle's expert choice held fixed
+# ---------------------------------------------------------------------------------------
+def _torch_layer_grads(inputs, dout):
+    sh = inputs["shape"]
+    t = lambda a: torch.tensor(oracle.bf16_to_f64(a), dtype=torch.float64, requires_grad=True)
+    x, wr, w13, w2 = t(inputs["x"]), t(inputs["w_router"]), t(inputs["w13"]), t(inputs["w2"])
+    ws13 = t(inputs["ws13"]) if sh.F_shared else None
+    ws2 = t(inputs["ws2"]) if sh.F_shared else None
+    res = oracle.layer_forward(inputs)                        # expert choice (held fixed)
+    idx = torch.tensor(res["topk_idx"].astype(np.int64))
+    logits = x @ wr.T
+    if sh.gate == wl.GATE_SOFTMAX:
+        keys = logits + (torch.tensor(inputs["bias"], dtype=torch.float64) if inputs.get("bias") is not None else 0)
+        sel = keys.gather(1, idx)
+        if sh.renormalize:
+            gates = torch.softmax(sel, dim=1)
+        else:
+            gates = torch.softmax(keys, dim=1).gather(1, idx)
+    else:
+        keys = torch.sigmoid(logits)
+        sel = keys.gather(1, idx)
+        gates = sel / sel.sum(dim=1, keepdim=True) if sh.renormalize else sel
+    gates = gates * sh.routed_scale
+    keep = torch.tensor(oracle.keep_mask(res["topk_idx"], sh.e_begin, sh.E_local, sh.expert_capacity))
+    F = sh.F
+    out = torch.zeros_like(x)
+    for tok in range(sh.T):
+        for j in range(sh.top_k):
+            e = int(idx[tok, j]) - sh.e_begin
+            if not keep[tok, j]:
+                continue
+            h = w13[e, :F] @ x[tok]
+            u = w13[e, F:] @ x[tok]
+            out[tok] = out[tok] + gates[tok, j] * (w2[e] @ (torch.nn.functional.silu(h) * u))
+    if sh.F_shared:
+        Fs = sh.F_shared
+        out = out + (torch.nn.functional.silu(x @ ws13[:Fs].T) * (x @ ws13[Fs:].T)) @ ws2.T
+    out.backward(torch.tensor(dout, dtype=torch.float64))
+    g = {"dx": x.grad, "dw_router": wr.grad, "dw13": w13.grad, "dw2": w2.grad}
+    if sh.F_shared:
+        g["dws13"], g["dws2"] = ws13.grad, ws2.grad
+    return {k: v.numpy() for k, v in g.items()}
+
+
+LAYER_CASES = {
+    "softmax_bias_renorm": (wl.MoEShape(T=9, d=12, E=6, top_k=2, F=5, E_local=6), 1.0),
+    "softmax_full_scaled": (wl.MoEShape(T=8, d=10, E=5, top_k=3, F=4, E_local=5, renormalize=0, routed_scale=1.5),
+                            0.0),
+    "sigmoid_groups_shared_slice": (wl.MoEShape(T=10, d=16, E=8, top_k=3, F=6, E_local=4, e_begin=2, F_shared=4,
+                                                gate=wl.GATE_SIGMOID, n_group=4, topk_group=2, routed_scale=2.5), 0.0),
+    "sigmoid_raw": (wl.MoEShape(T=7, d=8, E=6, top_k=2, F=4, E_local=6, gate=wl.GATE_SIGMOID, renormalize=0), 0.0),
+    "masked_capacity_drops": (wl.MoEShape(T=12, d=8, E=4, top_k=2, F=4, E_local=4, expert_capacity=3), 0.0),
+}
+
+
+@pytest.mark.parametrize("name", list(LAYER_CASES))
+def test_layer_backward_matches_torch_autograd(name):
+    sh, zipf = LAYER_CASES[name]
+    inputs = wl.custom_inputs(sh, seed=31, router_std=1.0, zipf_s=zipf)
+    if name == "softmax_bias_renorm":
+        inputs["bias"] = np.linspace(-0.5, 0.7, sh.E).astype(np.float32)
+    dout = np.random.default_rng(5).standard_normal((sh.T, sh.d))
+    got = bwd.layer_backward(inputs, dout)
+    ref = _torch_layer_grads(inputs, dout)
+    for key, val in ref.items():
+        np.testing.assert_allclose(got[key], val, rtol=1e-10, atol=1e-11, err_msg=key)
+
+
+def test_layer_backward_finite_differences():
+    """dx and dW_router against central differences of <dout, out> (the expert choice is
+    checked to be unchanged by every perturbation)."""
+    sh = wl.MoEShape(T=4, d=6, E=4, top_k=2, F=3, E_local=4, F_shared=2, gate=wl.GATE_SIGMOID)
+    inputs = wl.custom_inputs(sh, seed=7, router_std=1.0)
+    dout = np.random.default_rng(8).standard_normal((sh.T, sh.d))
+    got = bwd.layer_backward(inputs, dout)
+    base_idx = oracle.layer_forward(inputs)["topk_idx"]
+    xd = oracle.bf16_to_f64(inputs["x"])
+    wr = oracle.bf16_to_f64(inputs["w_router"])
+
+    def loss(xv, wrv):
+        idx, w, _ = oracle.route(xv, wrv, sh)
+        assert (idx == base_idx).all()
+        out = oracle.expert_outputs_for_tokens(xv, idx, w, sh, inputs["w13"], inputs["w2"], inputs["ws13"],
+                                               inputs["ws2"])
+        return float((dout * out).sum())
+
+    eps = 1e-6
+    for name, arr, grad in (("dx", xd, got["dx"]), ("dw_router", wr, got["dw_router"])):
+        num = np.zeros_like(arr)
+        for ix in np.ndindex(arr.shape):
+            a, b = arr.copy(), arr.copy()
+            a[ix] += eps
+            b[ix] -= eps
+            num[ix] = (loss(a, wr) - loss(b, wr)) / (2 * eps) if name == "dx" else \
+                (loss(xd, a) - loss(xd, b)) / (2 * eps)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7, err_msg=name)
