@@ -288,6 +288,42 @@ def backward_run(workload, steps):
                 "backward_frac_of_bf16_peak": 16.0 * unit / (t_bwd * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
 
+def layer_backward_run(workload, steps):
+    """The whole layer backward (moe_layer_backward) after one forward of the workload: per-call
+    time (warmup 10, median of 3 round medians of `steps` calls) next to the forward's, and the
+    executed MFMA work: expert and shared MLP backward 16 d F rows each (dA 2, recomputed
+    up-projection 4, dX 4, dW2 2, dW13 4), router 4 T E d (dx and dw_router)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    inputs = wl.make_inputs(workload)
+    sh = inputs["shape"]
+    layer = moe.DeviceLayer(inputs, device="cuda:0")
+    layer.forward()
+    torch.cuda.synchronize()
+    g = torch.Generator(device="cuda:0").manual_seed(9)
+    dout = torch.randn((sh.T, sh.d), generator=g, device="cuda:0").to(torch.bfloat16)
+    grads = layer.backward(dout)
+    t_bwd = timed_median(lambda: layer.backward(dout), steps)
+    t_fwd = timed_median(layer.forward, steps)
+    assert bool(torch.isfinite(grads["dx"].float()).all()) and bool(torch.isfinite(grads["dw13"].float()).all())
+    offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
+    n_loc = int(offsets[-1]) if sh.expert_capacity == 0 else int(
+        np.minimum(layer.region(moe.MOE_REGION_COUNTS, torch.int32, (sh.E_local,)).cpu().numpy(),
+                   sh.expert_capacity).sum())
+    d, F, Fs, T, E = sh.d, sh.F, sh.F_shared, sh.T, sh.E
+    executed = 16.0 * d * (F * n_loc + Fs * T) + 4.0 * T * E * d
+    fwd_flops = 6.0 * d * (F * n_loc + Fs * T) + 2.0 * T * E * d
+    log(f"layer backward {t_bwd * 1e3:.1f} us, forward {t_fwd * 1e3:.1f} us on {n_loc} local rows")
+    return sh, {"local_rows": n_loc, "backward_us": t_bwd * 1e3, "forward_us": t_fwd * 1e3,
+                "backward_tokens_per_s": T / (t_bwd * 1e-3),
+                "backward_tflops_executed": executed / (t_bwd * 1e-3) / 1e12,
+                "backward_frac_of_bf16_peak": executed / (t_bwd * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                "forward_tflops": fwd_flops / (t_fwd * 1e-3) / 1e12}
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -330,6 +366,8 @@ def main():
                     help="time the layer of --workload in the four fuse_gather x fuse_combine structures")
     ap.add_argument("--backward", action="store_true",
                     help="time the expert-MLP backward on one routed batch of --workload")
+    ap.add_argument("--layer-backward", action="store_true",
+                    help="time the whole layer backward (moe_layer_backward) of --workload")
     ap.add_argument("--capacity", type=int, default=0,
                     help="expert capacity of --masked-decode (0: T, every slot kept)")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
@@ -379,6 +417,17 @@ def main():
                           "data": "synthetic", "vs_baseline": None,
                           "config": {"workload": args.workload, "T": sh.T, "d": sh.d, "E": sh.E, "top_k": sh.top_k,
                                      "E_local": sh.E_local, "F": sh.F},
+                          "protocol": "warmup 10; median of 3 round medians of the per-call event times",
+                          **row}), flush=True)
+        return
+    if args.layer_backward:
+        sh, row = layer_backward_run(args.workload, max(args.steps, 10))
+        print(json.dumps({"metric": "MoE-layer backward (dx, dw_router, expert and shared dW) latency and TFLOP/s, "
+                                    "1 MI355X",
+                          "unit": "us", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "config": {"workload": args.workload, "T": sh.T, "d": sh.d, "E": sh.E, "top_k": sh.top_k,
+                                     "E_local": sh.E_local, "F": sh.F, "F_shared": sh.F_shared},
                           "protocol": "warmup 10; median of 3 round medians of the per-call event times",
                           **row}), flush=True)
         return

@@ -73,7 +73,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 4
+#define MOE_ABI_VERSION 5
 
 /* moe_shape_t.fusion: which of the paper's four kernel structures moe_layer_forward runs
  * (Section 4, kernel generation: fuse_gather folds the token permute into the first GEMM's
@@ -105,7 +105,8 @@ typedef enum moe_ws_kind {
   MOE_WS_PERMUTE = 1,
   MOE_WS_FFN = 2,
   MOE_WS_LAYER = 3,
-  MOE_WS_FFN_BWD = 4
+  MOE_WS_FFN_BWD = 4,
+  MOE_WS_LAYER_BWD = 5
 } moe_ws_kind_t;
 
 /* Named regions inside a MOE_WS_LAYER workspace (moe_workspace_offset). */
@@ -226,6 +227,38 @@ int moe_grouped_ffn_backward(const moe_shape_t* shape, const void* x_perm, const
                              const void* w13, const void* w2, const void* dy_perm,
                              void* dx_perm, void* dw13, void* dw2,
                              void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the whole layer (the paper's training leg, Section 4, engine registration: the
+ * forward composes the expert kernels' two GEMMs, the backward their dual GEMMs), for the
+ * output gradient dout [T, d] of the moe_layer_forward call that left its state in fwd_ws
+ * (same shape and inputs; the choice of experts is that forward's and carries no gradient):
+ *   dgate[t, j] = <dout[t], y_perm[row(t, j)]>            (local slots; 0 for the others)
+ *   expert rows: dy_perm[row(t, j)] = topk_w[t, j] dout[t], then the expert-MLP backward
+ *                (as moe_grouped_ffn_backward) -> dx rows, dw13, dw2
+ *   shared expert: its MLP backward for dout on every token -> dx rows, dws13, dws2
+ *   gates -> router logits: d key from dgate by the derivative of the gate formula
+ *                (shape->gate / renormalize / routed_scale; see moe_gate_t), times
+ *                k (1 - k) for sigmoid keys; the keys are recomputed bit-identically from
+ *                the forward's float32 logit partials
+ *   router: dx += dlogits w_router,  dw_router = dlogits^T x
+ *   dx[t] = bf16( sum of the token's expert-row gradients (slot order) + shared + router ),
+ *           float32 accumulation, one rounding.
+ * A router bias is a constant (no gradient).  Outputs: dx [T, d], dw_router [E, d],
+ * dw13 [E_local, 2F, d], dw2 [E_local, d, F], dws13 [2F_s, d], dws2 [d, F_s] (the last two
+ * only when F_shared > 0), all bf16 and written in full (an expert without rows gets zeros).
+ * Rounded to bf16 once each on the way: dlogits, the expert rows' output gradients, and the
+ * expert-MLP backward's intermediates (as moe_grouped_ffn_backward).
+ * fwd_ws / fwd_ws_bytes: the MOE_WS_LAYER workspace of that forward, whose routing,
+ * permutation, logit partials and expert output rows are read; the forward must not have
+ * folded the combine (MOE_FUSE_COMBINE leaves no expert output rows: MOE_ERR_UNSUPPORTED).
+ * The backward writes the forward's MOE_REGION_X_PERM region (the expert-ordered token rows).
+ * Also requires E % 8 == 0 (the router GEMMs reduce over, and produce, rows of E values).
+ * ws: MOE_WS_LAYER_BWD bytes (gradient rows and GEMM intermediates). */
+int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                       const void* w13, const void* w2, const void* ws13, const void* ws2,
+                       const void* dout, void* fwd_ws, size_t fwd_ws_bytes,
+                       void* dx, void* dw_router, void* dw13, void* dw2, void* dws13, void* dws2,
+                       void* ws, size_t ws_bytes, void* stream);
 
 /* Gate-weighted combine (steps 10-11):
  *   out[t] = bf16( sum over slots j with slot_row[t,j] >= 0 of topk_w[t,j] * y_perm[slot_row[t,j]]

@@ -19,7 +19,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmoe_mi355x.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "gemm.hip", "gemm_bwd.hip", "route.hip", "permute.hip", "combine.hip"]
+SOURCES = ["api.cpp", "gemm.hip", "gemm_bwd.hip", "route.hip", "permute.hip", "combine.hip",
+           "layer_bwd.hip"]
 
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          # keep the compiler from emitting packed fp32 VALU ops (v_pk_*_f32)

@@ -154,6 +154,36 @@ LayerLayout layer_layout(const moe_shape_t* s) {
   return L;
 }
 
+// Layer backward: gate gradients, logit gradients, the expert rows' output and input
+// gradients, the shared expert's and the router's input gradients, and the expert-MLP
+// backward's intermediates (routed and shared run one after the other on the same scratch).
+struct LayerBwdLayout {
+  size_t seg, dgate, dlogits, dy_perm, dx_perm, dx_shared, dx_router, scratch;
+  size_t total;
+};
+
+LayerBwdLayout layer_bwd_layout(const moe_shape_t* s) {
+  LayerBwdLayout L{};
+  const size_t T = (size_t)s->T, k = (size_t)s->top_k, cap = (size_t)capacity(s), d = (size_t)s->d;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  L.seg = take(2 * sizeof(int32_t));
+  L.dgate = take(T * k * 4);
+  L.dlogits = take(T * (size_t)s->E * 2);
+  L.dy_perm = take(cap * d * 2);
+  L.dx_perm = take(cap * d * 2);
+  L.dx_shared = take(s->F_shared > 0 ? T * d * 2 : 0);
+  L.dx_router = take(T * d * 2);
+  // ffn_backward takes four planes of align_up(rows * F * 2) bytes
+  L.scratch = take(std::max(4 * align_up(cap * (size_t)s->F * 2), 4 * align_up(T * (size_t)s->F_shared * 2)));
+  L.total = off;
+  return L;
+}
+
 size_t ws_need(const moe_shape_t* s, int kind) {
   switch (kind) {
     case MOE_WS_ROUTE: return ws_route(s);
@@ -161,6 +191,7 @@ size_t ws_need(const moe_shape_t* s, int kind) {
     case MOE_WS_FFN: return ws_ffn(s);
     case MOE_WS_LAYER: return layer_layout(s).total;
     case MOE_WS_FFN_BWD: return ws_ffn_bwd(s);
+    case MOE_WS_LAYER_BWD: return layer_bwd_layout(s).total;
     default: return 0;
   }
 }
@@ -366,45 +397,57 @@ int do_combine(const moe_shape_t* s, const void* y_perm, const int32_t* slot_row
 
 // Expert-MLP backward (arguments validated): dA = dY W2, the up-projection recomputed with
 // the SwiGLU-backward epilogue, dX = [dH dU] w13, dW2 = dY^T A, dW13 = [dH dU]^T X.
-int do_ffn_backward(const moe_shape_t* s, const void* x_perm, const int32_t* offsets, const void* w13,
-                    const void* w2, const void* dy, void* dx, void* dw13, void* dw2, void* ws, hipStream_t st) {
-  const int64_t cap = capacity(s);
-  const int d = s->d, F = s->F, E = s->E_local, C = s->expert_capacity;
-  auto* da = at<moe::bf16_t>(ws, 0);
-  auto* act = at<moe::bf16_t>(ws, ws_ffn(s));
-  auto* dhu = at<moe::bf16_t>(ws, 2 * ws_ffn(s));
-  const int64_t rows_hint = std::max<int64_t>(1, cap / E);
+// Group g owns rows [offsets[g], offsets[g+1]) of x / dy / dx (or, with seg_stride > 0, the
+// first min(offsets[g], seg_stride) rows of [g seg_stride, (g+1) seg_stride)); `rows` bounds
+// them; scratch holds 4 rows x F bf16 values (dA, activation, [dH dU]).
+struct FfnBwd {
+  const void* x = nullptr;
+  const int32_t* offsets = nullptr;
+  int groups = 0;
+  int64_t rows = 0, rows_hint = 0;
+  int seg_stride = 0, d = 0, F = 0;
+  bool any_rows = true;       // false: no token rows (only the weight gradients, all zero)
+  const void *w13 = nullptr, *w2 = nullptr, *dy = nullptr;
+  void *dx = nullptr, *dw13 = nullptr, *dw2 = nullptr, *scratch = nullptr;
+};
+
+int ffn_backward(const FfnBwd& a, hipStream_t st) {
+  const int d = a.d, F = a.F;
+  const size_t plane = align_up((size_t)a.rows * F * sizeof(uint16_t));
+  auto* da = at<moe::bf16_t>(a.scratch, 0);
+  auto* act = at<moe::bf16_t>(a.scratch, plane);
+  auto* dhu = at<moe::bf16_t>(a.scratch, 2 * plane);
   moe::GemmBwdProblem g{};
-  g.offsets = offsets;
-  g.groups = E;
-  g.seg_stride = C;
-  g.max_rows = cap;
-  g.rows_hint = rows_hint;
+  g.offsets = a.offsets;
+  g.groups = a.groups;
+  g.seg_stride = a.seg_stride;
+  g.max_rows = a.rows;
+  g.rows_hint = a.rows_hint;
   // dA = dY W2 (W2 [d][F] read as the transposed operand)
   g.mode = moe::BWD_ROWS;
   g.x_mn = false;
   g.w_mn = true;
-  g.X = static_cast<const moe::bf16_t*>(dy);
+  g.X = static_cast<const moe::bf16_t*>(a.dy);
   g.ldx = d;
-  g.W = static_cast<const moe::bf16_t*>(w2);
+  g.W = static_cast<const moe::bf16_t*>(a.w2);
   g.ldw = F;
   g.w_group_stride = (int64_t)d * F;
   g.N = F;
   g.K = d;
   g.Y = da;
   g.ldy = F;
-  if (s->T > 0) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dA launch"));
+  if (a.any_rows) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dA launch"));
   // recompute H, U; dH, dU and the activation from dA
   moe::GemmProblem up{};
-  up.X = static_cast<const moe::bf16_t*>(x_perm);
+  up.X = static_cast<const moe::bf16_t*>(a.x);
   up.ldx = d;
-  up.offsets = offsets;
-  up.groups = E;
-  up.rows_single = cap;
-  up.max_rows = cap;
-  up.seg_stride = C;
-  up.rows_hint = rows_hint;
-  up.W = static_cast<const moe::bf16_t*>(w13);
+  up.offsets = a.offsets;
+  up.groups = a.groups;
+  up.rows_single = a.rows;
+  up.max_rows = a.rows;
+  up.seg_stride = a.seg_stride;
+  up.rows_hint = a.rows_hint;
+  up.W = static_cast<const moe::bf16_t*>(a.w13);
   up.w_group_stride = (int64_t)2 * F * d;
   up.N = F;
   up.K = d;
@@ -413,18 +456,18 @@ int do_ffn_backward(const moe_shape_t* s, const void* x_perm, const int32_t* off
   up.epi = moe::EPI_SWIGLU_BWD;
   up.dact = da;
   up.act_out = act;
-  if (s->T > 0) CHECK(hip_status(moe::launch_grouped_gemm(up, st), "SwiGLU backward launch"));
+  if (a.any_rows) CHECK(hip_status(moe::launch_grouped_gemm(up, st), "SwiGLU backward launch"));
   // dX = [dH dU] w13 (w13 [2F][d] read as the transposed operand)
   g.X = dhu;
   g.ldx = 2 * F;
-  g.W = static_cast<const moe::bf16_t*>(w13);
+  g.W = static_cast<const moe::bf16_t*>(a.w13);
   g.ldw = d;
   g.w_group_stride = (int64_t)2 * F * d;
   g.N = d;
   g.K = 2 * F;
-  g.Y = static_cast<moe::bf16_t*>(dx);
+  g.Y = static_cast<moe::bf16_t*>(a.dx);
   g.ldy = d;
-  if (s->T > 0) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dX launch"));
+  if (a.any_rows) CHECK(hip_status(moe::launch_gemm_bwd(g, st), "dX launch"));
   // weight gradients: reductions over each expert's rows (also with no tokens: then every
   // segment is empty and the launches write zeros)
   moe::GemmBwdProblem w = g;
@@ -432,27 +475,49 @@ int do_ffn_backward(const moe_shape_t* s, const void* x_perm, const int32_t* off
   w.x_mn = w.w_mn = true;
   w.w_group_stride = 0;
   // dW2[e] = dY^T A: [d, F]
-  w.X = static_cast<const moe::bf16_t*>(dy);
+  w.X = static_cast<const moe::bf16_t*>(a.dy);
   w.ldx = d;
   w.W = act;
   w.ldw = F;
   w.M = d;
   w.N = F;
-  w.Y = static_cast<moe::bf16_t*>(dw2);
+  w.Y = static_cast<moe::bf16_t*>(a.dw2);
   w.ldy = F;
   w.y_group_stride = (int64_t)d * F;
   CHECK(hip_status(moe::launch_gemm_bwd(w, st), "dW2 launch"));
   // dW13[e] = [dH dU]^T X: [2F, d]
   w.X = dhu;
   w.ldx = 2 * F;
-  w.W = static_cast<const moe::bf16_t*>(x_perm);
+  w.W = static_cast<const moe::bf16_t*>(a.x);
   w.ldw = d;
   w.M = 2 * F;
   w.N = d;
-  w.Y = static_cast<moe::bf16_t*>(dw13);
+  w.Y = static_cast<moe::bf16_t*>(a.dw13);
   w.ldy = d;
   w.y_group_stride = (int64_t)2 * F * d;
   return hip_status(moe::launch_gemm_bwd(w, st), "dW13 launch");
+}
+
+int do_ffn_backward(const moe_shape_t* s, const void* x_perm, const int32_t* offsets, const void* w13,
+                    const void* w2, const void* dy, void* dx, void* dw13, void* dw2, void* ws, hipStream_t st) {
+  FfnBwd a;
+  a.x = x_perm;
+  a.offsets = offsets;
+  a.groups = s->E_local;
+  a.rows = capacity(s);
+  a.any_rows = s->T > 0;
+  a.rows_hint = std::max<int64_t>(1, capacity(s) / s->E_local);
+  a.seg_stride = s->expert_capacity;
+  a.d = s->d;
+  a.F = s->F;
+  a.w13 = w13;
+  a.w2 = w2;
+  a.dy = dy;
+  a.dx = dx;
+  a.dw13 = dw13;
+  a.dw2 = dw2;
+  a.scratch = ws;
+  return ffn_backward(a, st);
 }
 
 }  // namespace
@@ -476,7 +541,7 @@ const char* moe_last_error(void) { return g_err.c_str(); }
 
 size_t moe_workspace_size(const moe_shape_t* shape, int kind) {
   if (check_shape(shape) != MOE_OK) return 0;
-  if (kind < MOE_WS_ROUTE || kind > MOE_WS_FFN_BWD) {
+  if (kind < MOE_WS_ROUTE || kind > MOE_WS_LAYER_BWD) {
     fail(MOE_ERR_INVALID_ARG, "workspace kind (%d) unknown", kind);
     return 0;
   }
@@ -561,6 +626,205 @@ int moe_grouped_ffn_backward(const moe_shape_t* shape, const void* x_perm, const
     CHECK(check_ptr(dx_perm, 16, "dx_perm"));
   }
   CHECK(do_ffn_backward(shape, x_perm, offsets, w13, w2, dy_perm, dx_perm, dw13, dw2, ws, as_stream(stream)));
+  return ok();
+}
+
+int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
+                       const void* w13, const void* w2, const void* ws13, const void* ws2, const void* dout,
+                       void* fwd_ws, size_t fwd_ws_bytes, void* dx, void* dw_router, void* dw13, void* dw2,
+                       void* dws13, void* dws2, void* ws, size_t ws_bytes, void* stream) {
+  CHECK(check_shape(shape));
+  const moe_shape_t* s = shape;
+  if (s->E_local > moe::kMaxGroups) return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", s->E_local, moe::kMaxGroups);
+  if (bias && s->gate != MOE_GATE_SOFTMAX)
+    return fail(MOE_ERR_UNSUPPORTED, "a router bias is only defined for softmax gating");
+  if (fuse_combine(s))
+    return fail(MOE_ERR_UNSUPPORTED,
+                "the forward folded the combine (MOE_FUSE_COMBINE): it leaves no expert output rows for the gate "
+                "gradients");
+  if (s->E % 8)
+    return fail(MOE_ERR_UNSUPPORTED, "E (%d) %% 8 != 0 (the router backward GEMMs take rows of E values)", s->E);
+  CHECK(check_ptr(dw_router, 16, "dw_router"));
+  CHECK(check_ptr(dw13, 16, "dw13"));
+  CHECK(check_ptr(dw2, 16, "dw2"));
+  if (s->F_shared > 0) {
+    CHECK(check_ptr(dws13, 16, "dws13"));
+    CHECK(check_ptr(dws2, 16, "dws2"));
+  }
+  hipStream_t st = as_stream(stream);
+  const int64_t T = s->T;
+  const int d = s->d, E = s->E, F = s->F, Fs = s->F_shared;
+  if (T == 0) {
+    // no tokens: every weight gradient is zero (bf16 zero = all-zero bits)
+    auto zero = [&](void* p, int64_t elems, const char* what) {
+      return hip_status(moe::launch_zero_f32(static_cast<float*>(p), elems / 2, st), what);
+    };
+    CHECK(zero(dw_router, (int64_t)E * d, "dw_router clear launch"));
+    CHECK(zero(dw13, (int64_t)s->E_local * 2 * F * d, "dw13 clear launch"));
+    CHECK(zero(dw2, (int64_t)s->E_local * d * F, "dw2 clear launch"));
+    if (Fs > 0) {
+      CHECK(zero(dws13, (int64_t)2 * Fs * d, "dws13 clear launch"));
+      CHECK(zero(dws2, (int64_t)d * Fs, "dws2 clear launch"));
+    }
+    return ok();
+  }
+  CHECK(check_ptr(x, 16, "x"));
+  CHECK(check_ptr(w_router, 16, "w_router"));
+  if (bias) CHECK(check_ptr(bias, 4, "bias"));
+  CHECK(check_ptr(w13, 16, "w13"));
+  CHECK(check_ptr(w2, 16, "w2"));
+  if (Fs > 0) {
+    CHECK(check_ptr(ws13, 16, "ws13"));
+    CHECK(check_ptr(ws2, 16, "ws2"));
+  }
+  CHECK(check_ptr(dout, 16, "dout"));
+  CHECK(check_ptr(dx, 16, "dx"));
+  CHECK(check_ws(s, MOE_WS_LAYER, fwd_ws, fwd_ws_bytes));
+  CHECK(check_ws(s, MOE_WS_LAYER_BWD, ws, ws_bytes));
+
+  const LayerLayout F0 = layer_layout(s);
+  const LayerBwdLayout B = layer_bwd_layout(s);
+  const int32_t* topk_idx = at<int32_t>(fwd_ws, F0.region[MOE_REGION_TOPK_IDX]);
+  const float* topk_w = at<float>(fwd_ws, F0.region[MOE_REGION_TOPK_W]);
+  const int32_t* counts = at<int32_t>(fwd_ws, F0.region[MOE_REGION_COUNTS]);
+  const int32_t* offsets = at<int32_t>(fwd_ws, F0.region[MOE_REGION_OFFSETS]);
+  const int32_t* slot_row = at<int32_t>(fwd_ws, F0.region[MOE_REGION_SLOT_ROW]);
+  auto* x_perm = at<moe::bf16_t>(fwd_ws, F0.region[MOE_REGION_X_PERM]);
+  const auto* y_perm = at<moe::bf16_t>(fwd_ws, F0.region[MOE_REGION_Y_PERM]);
+  int32_t* seg = at<int32_t>(ws, B.seg);
+  float* dgate = at<float>(ws, B.dgate);
+  auto* dlogits = at<moe::bf16_t>(ws, B.dlogits);
+  auto* dy_perm = at<moe::bf16_t>(ws, B.dy_perm);
+  auto* dx_perm = at<moe::bf16_t>(ws, B.dx_perm);
+  auto* dx_shared = Fs > 0 ? at<moe::bf16_t>(ws, B.dx_shared) : nullptr;
+  auto* dx_router = at<moe::bf16_t>(ws, B.dx_router);
+  void* scratch = at<void>(ws, B.scratch);
+  const int64_t cap = capacity(s);
+  const int C = s->expert_capacity;
+
+  // combine backward: gate gradients and the expert rows' output gradients
+  moe::CombineBwdProblem cb{};
+  cb.dout = static_cast<const moe::bf16_t*>(dout);
+  cb.y_perm = y_perm;
+  cb.slot_row = slot_row;
+  cb.topk_w = topk_w;
+  cb.dgate = dgate;
+  cb.dy_perm = dy_perm;
+  cb.T = T;
+  cb.cap = cap;
+  cb.d = d;
+  cb.top_k = s->top_k;
+  CHECK(hip_status(moe::launch_combine_bwd(cb, st), "combine backward launch"));
+  // gates -> logits (keys recomputed from the forward's partials); also the {0, T} segment
+  moe::GateBwdProblem gb{};
+  gb.logits = at<float>(fwd_ws, F0.logits);
+  gb.nsplit = moe::logits_splits(T, E, d);
+  gb.split_stride = T * (int64_t)E;
+  gb.bias = bias;
+  gb.topk_idx = topk_idx;
+  gb.dgate = dgate;
+  gb.T = T;
+  gb.E = E;
+  gb.top_k = s->top_k;
+  gb.gate = s->gate;
+  gb.renormalize = s->renormalize;
+  gb.routed_scale = s->routed_scale;
+  gb.dlogits = dlogits;
+  gb.seg = seg;
+  CHECK(hip_status(moe::launch_gate_bwd(gb, st), "gate backward launch"));
+  // expert-ordered token rows (the forward may have read them straight from x)
+  moe::PermuteProblem pp{};
+  pp.x = static_cast<const moe::bf16_t*>(x);
+  pp.T = T;
+  pp.d = d;
+  pp.top_k = s->top_k;
+  pp.slot_row = const_cast<int32_t*>(slot_row);
+  pp.x_perm = x_perm;
+  pp.cap = cap;
+  CHECK(hip_status(moe::launch_gather(pp, st), "row gather launch"));
+  // routed experts
+  FfnBwd r;
+  r.x = x_perm;
+  r.offsets = C > 0 ? counts : offsets;
+  r.groups = s->E_local;
+  r.rows = cap;
+  int64_t hint = std::max<int64_t>(1, T * s->top_k / E);
+  if (C > 0) hint = std::min<int64_t>(hint, C);
+  r.rows_hint = hint;
+  r.seg_stride = C;
+  r.d = d;
+  r.F = F;
+  r.w13 = w13;
+  r.w2 = w2;
+  r.dy = dy_perm;
+  r.dx = dx_perm;
+  r.dw13 = dw13;
+  r.dw2 = dw2;
+  r.scratch = scratch;
+  CHECK(ffn_backward(r, st));
+  // shared expert: one segment of all T token rows, output gradient dout itself
+  if (Fs > 0) {
+    FfnBwd h;
+    h.x = x;
+    h.offsets = seg;
+    h.groups = 1;
+    h.rows = T;
+    h.rows_hint = T;
+    h.d = d;
+    h.F = Fs;
+    h.w13 = ws13;
+    h.w2 = ws2;
+    h.dy = dout;
+    h.dx = dx_shared;
+    h.dw13 = dws13;
+    h.dw2 = dws2;
+    h.scratch = scratch;
+    CHECK(ffn_backward(h, st));
+  }
+  // router: dx_router = dlogits w_router (w_router [E][d] read as the transposed operand)
+  moe::GemmBwdProblem g{};
+  g.mode = moe::BWD_ROWS;
+  g.x_mn = false;
+  g.w_mn = true;
+  g.offsets = seg;
+  g.groups = 1;
+  g.max_rows = T;
+  g.rows_hint = T;
+  g.X = dlogits;
+  g.ldx = E;
+  g.W = static_cast<const moe::bf16_t*>(w_router);
+  g.ldw = d;
+  g.N = d;
+  g.K = E;
+  g.Y = dx_router;
+  g.ldy = d;
+  CHECK(hip_status(moe::launch_gemm_bwd(g, st), "router dx launch"));
+  // dw_router = dlogits^T x: one reduction over all T token rows
+  moe::GemmBwdProblem w = g;
+  w.mode = moe::BWD_KSEG;
+  w.x_mn = w.w_mn = true;
+  w.X = dlogits;
+  w.ldx = E;
+  w.W = static_cast<const moe::bf16_t*>(x);
+  w.ldw = d;
+  w.M = E;
+  w.N = d;
+  w.Y = static_cast<moe::bf16_t*>(dw_router);
+  w.ldy = d;
+  w.y_group_stride = 0;
+  CHECK(hip_status(moe::launch_gemm_bwd(w, st), "router weight gradient launch"));
+  // dx: the token's expert-row gradients in slot order, then the shared expert's, then the router's
+  moe::UnpermuteSumProblem u{};
+  u.rows = dx_perm;
+  u.slot_row = slot_row;
+  u.extra0 = dx_shared;
+  u.extra1 = dx_router;
+  u.out = static_cast<moe::bf16_t*>(dx);
+  u.T = T;
+  u.cap = cap;
+  u.d = d;
+  u.top_k = s->top_k;
+  CHECK(hip_status(moe::launch_unpermute_sum(u, st), "row gradient sum launch"));
   return ok();
 }
 

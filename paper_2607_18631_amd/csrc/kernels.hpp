@@ -158,6 +158,53 @@ struct CombineProblem {
 };
 hipError_t launch_combine(const CombineProblem& p, hipStream_t stream);
 
+// The row copy of the permutation alone: x_perm[slot_row[t, j]] = x[t] for every local slot.
+hipError_t launch_gather(const PermuteProblem& p, hipStream_t stream);
+
+// ---- layer backward (around the expert-MLP backward GEMMs) ----
+// dgate[t, j] = <dout[t], y_perm[slot_row[t, j]]> (0 for a slot without a local row) and
+// dy_perm[slot_row[t, j]] = bf16(topk_w[t, j] * dout[t]).
+struct CombineBwdProblem {
+  const bf16_t* dout;         // [T, d]
+  const bf16_t* y_perm;       // [cap, d]
+  const int32_t* slot_row;    // [T, top_k]
+  const float* topk_w;        // [T, top_k]
+  float* dgate;               // [T, top_k]
+  bf16_t* dy_perm;            // [cap, d]
+  int64_t T, cap;
+  int32_t d, top_k;
+};
+hipError_t launch_combine_bwd(const CombineBwdProblem& p, hipStream_t stream);
+
+// dlogits [T, E] = d loss / d router logit (bf16), from the gate gradients and the forward's
+// float32 keys recomputed from its logit partials; also writes seg = {0, T}.
+struct GateBwdProblem {
+  const float* logits;        // nsplit partials [T, E] of the forward's router GEMM
+  int32_t nsplit;
+  int64_t split_stride;
+  const float* bias;          // [E] or nullptr (softmax keys)
+  const int32_t* topk_idx;    // [T, top_k]
+  const float* dgate;         // [T, top_k]
+  int64_t T;
+  int32_t E, top_k, gate, renormalize;
+  float routed_scale;
+  bf16_t* dlogits;            // [T, E]
+  int32_t* seg;               // [2] or nullptr
+};
+hipError_t launch_gate_bwd(const GateBwdProblem& p, hipStream_t stream);
+
+// out[t] = bf16( sum of rows[slot_row[t, j]] over the local slots (slot order) + extra0[t] + extra1[t] )
+struct UnpermuteSumProblem {
+  const bf16_t* rows;         // [cap, d]
+  const int32_t* slot_row;    // [T, top_k]
+  const bf16_t* extra0;       // [T, d] or nullptr
+  const bf16_t* extra1;       // [T, d] or nullptr
+  bf16_t* out;                // [T, d]
+  int64_t T, cap;
+  int32_t d, top_k;
+};
+hipError_t launch_unpermute_sum(const UnpermuteSumProblem& p, hipStream_t stream);
+
 // acc[0 .. n) = 0 (a fill kernel, so the call can sit inside a captured graph); n % 4 == 0
 hipError_t launch_zero_f32(float* acc, int64_t n, hipStream_t stream);
 // out[i] = bf16(acc[i]) for i < n, n % 8 == 0

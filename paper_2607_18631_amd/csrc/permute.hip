@@ -248,4 +248,10 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*bet
   return hipGetLastError();
 }
 
+hipError_t launch_gather(const PermuteProblem& p, hipStream_t stream) {
+  if (p.T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather, dim3((unsigned)((p.T + 3) / 4)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
 }  // namespace moe

@@ -18,14 +18,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmoe_mi355x.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
-MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER, MOE_WS_FFN_BWD = range(5)
+MOE_WS_ROUTE, MOE_WS_PERMUTE, MOE_WS_FFN, MOE_WS_LAYER, MOE_WS_FFN_BWD, MOE_WS_LAYER_BWD = range(6)
 MOE_FUSION_SET, MOE_FUSE_GATHER, MOE_FUSE_COMBINE = 0x10, 0x1, 0x2
 (MOE_REGION_TOPK_IDX, MOE_REGION_TOPK_W, MOE_REGION_COUNTS, MOE_REGION_OFFSETS, MOE_REGION_ROW_TOKEN,
  MOE_REGION_SLOT_ROW, MOE_REGION_X_PERM, MOE_REGION_Y_PERM, MOE_REGION_SHARED_Y) = range(9)
 
 EXPORTS = ["moe_abi_version", "moe_status_string", "moe_last_error", "moe_workspace_size",
            "moe_workspace_offset", "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
-           "moe_layer_forward", "moe_layer_forward_traced", "moe_grouped_ffn_backward"]
+           "moe_layer_forward", "moe_layer_forward_traced", "moe_grouped_ffn_backward", "moe_layer_backward"]
 MOE_STEP_NAMES = ["router_gemm", "gate", "histogram", "permute", "ffn_up", "ffn_down", "shared_up",
                   "shared_down", "combine"]
 
@@ -71,11 +71,13 @@ def lib():
         L.moe_combine.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.moe_grouped_ffn_backward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                                _vp]
+        L.moe_layer_backward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_layer_forward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_layer_forward_traced.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                                ctypes.POINTER(_vp), _vp]
         for f in ("moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine", "moe_layer_forward",
-                  "moe_layer_forward_traced", "moe_grouped_ffn_backward"):
+                  "moe_layer_forward_traced", "moe_grouped_ffn_backward", "moe_layer_backward"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -149,6 +151,14 @@ def moe_grouped_ffn_backward(sh, x_perm, offsets, w13, w2, dy_perm, dx_perm, dw1
                                           0 if ws is None else ws.numel(), _stream(stream)))
 
 
+def moe_layer_backward(sh, x, w_router, bias, w13, w2, ws13, ws2, dout, fwd_ws, dx, dw_router, dw13, dw2, dws13,
+                       dws2, ws, stream=None):
+    _check(lib().moe_layer_backward(ctypes.byref(shape_c(sh)), _p(x), _p(w_router), _p(bias), _p(w13), _p(w2),
+                                    _p(ws13), _p(ws2), _p(dout), _p(fwd_ws), 0 if fwd_ws is None else fwd_ws.numel(),
+                                    _p(dx), _p(dw_router), _p(dw13), _p(dw2), _p(dws13), _p(dws2), _p(ws),
+                                    0 if ws is None else ws.numel(), _stream(stream)))
+
+
 def moe_combine(sh, y_perm, slot_row, topk_w, shared_y, out, stream=None):
     _check(lib().moe_combine(ctypes.byref(shape_c(sh)), _p(y_perm), _p(slot_row), _p(topk_w), _p(shared_y),
                              _p(out), _stream(stream)))
@@ -212,6 +222,26 @@ class DeviceLayer:
         moe_layer_forward_traced(self.shape, self.x, self.w_router, self.bias, self.w13, self.w2, self.ws13,
                                  self.ws2, self.out, self.ws, events, stream)
         return self.out
+
+    def backward(self, dout, stream=None):
+        """``moe_layer_backward`` for output gradient ``dout`` of the last ``forward()``; returns
+        the gradients as a dict of device tensors (dx, dw_router, dw13, dw2, dws13, dws2)."""
+        import torch
+        sh = self.shape
+        dev = self.device
+        bf = torch.bfloat16
+        g = {"dx": torch.empty((sh.T, sh.d), dtype=bf, device=dev),
+             "dw_router": torch.empty((sh.E, sh.d), dtype=bf, device=dev),
+             "dw13": torch.empty((sh.E_local, 2 * sh.F, sh.d), dtype=bf, device=dev),
+             "dw2": torch.empty((sh.E_local, sh.d, sh.F), dtype=bf, device=dev),
+             "dws13": torch.empty((2 * sh.F_shared, sh.d), dtype=bf, device=dev) if sh.F_shared > 0 else None,
+             "dws2": torch.empty((sh.d, sh.F_shared), dtype=bf, device=dev) if sh.F_shared > 0 else None}
+        if getattr(self, "ws_bwd", None) is None:
+            self.ws_bwd = alloc_workspace(sh, MOE_WS_LAYER_BWD, dev)
+        moe_layer_backward(sh, self.x, self.w_router, self.bias, self.w13, self.w2, self.ws13, self.ws2, dout,
+                           self.ws, g["dx"], g["dw_router"], g["dw13"], g["dw2"], g["dws13"], g["dws2"],
+                           self.ws_bwd, stream)
+        return g
 
     def region(self, region: int, dtype, shape):
         import torch

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(moe.EXPORTS), names
     for n in names:
         assert hasattr(L, n), n
-    assert L.moe_abi_version() == 4
+    assert L.moe_abi_version() == 5
 
 
 def test_status_strings():
@@ -72,7 +72,7 @@ def test_masked_layout_workspace():
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))
 def test_workspace_sizes(name):
     sh = wl.WORKLOADS[name].shape
-    for kind in range(5):
+    for kind in range(6):
         n = moe.workspace_size(sh, kind)
         assert n > 0 and n % 256 == 0
     layer = moe.workspace_size(sh, moe.MOE_WS_LAYER)
@@ -174,3 +174,49 @@ def test_zero_tokens_is_a_noop():
     sh = BASE.replace(T=0)
     st, msg = _layer_call(sh, x=None, wr=None, w13=None, w2=None, out=None, ws=None)
     assert st == moe.MOE_OK and msg == ""
+
+
+def _bwd_call(sh, dout=FAKE, fwd_ws=FAKE, fwd_bytes=1 << 44, dx=FAKE, dwr=FAKE, dw13=FAKE, dw2=FAKE, dws13=None,
+              dws2=None, ws=FAKE, ws_bytes=1 << 44, bias=None):
+    return _status(moe.lib().moe_layer_backward, ctypes.byref(moe.shape_c(sh)), FAKE, FAKE, bias, FAKE, FAKE,
+                   FAKE if sh.F_shared else None, FAKE if sh.F_shared else None, dout, fwd_ws, fwd_bytes, dx, dwr,
+                   dw13, dw2, dws13, dws2, ws, ws_bytes, None)
+
+
+def test_layer_backward_workspace():
+    """Gradient rows of the experts (cap x d, twice), the router and shared rows (T x d),
+    dlogits (T x E bf16), gate gradients and the expert-MLP backward's intermediates."""
+    for name in wl.WORKLOADS:
+        sh = wl.WORKLOADS[name].shape
+        need = moe.workspace_size(sh, moe.MOE_WS_LAYER_BWD)
+        cap, T, d = sh.capacity, sh.T, sh.d
+        low = 2 * cap * d * 2 + T * d * 2 * (2 if sh.F_shared else 1) + T * sh.E * 2 + T * sh.top_k * 4
+        low += max(4 * cap * sh.F * 2, 4 * T * sh.F_shared * 2)
+        assert need % 256 == 0 and need >= low, (name, need, low)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(fusion=wl.FUSION_VARIANTS["both"]), moe.MOE_ERR_UNSUPPORTED, "MOE_FUSE_COMBINE"),
+    (dict(E=12, E_local=12), moe.MOE_ERR_UNSUPPORTED, "E (12) % 8 != 0"),
+    (dict(F=12), moe.MOE_ERR_UNSUPPORTED, "F (12) % 8 != 0"),
+])
+def test_layer_backward_shape_validation(kw, status, needle):
+    st, msg = _bwd_call(BASE.replace(**kw))
+    assert st == status and needle in msg, (st, msg)
+
+
+def test_layer_backward_pointer_and_workspace_validation():
+    st, msg = _bwd_call(BASE, dout=None)
+    assert st == moe.MOE_ERR_INVALID_ARG and "dout is NULL" in msg
+    st, msg = _bwd_call(BASE, dwr=MISALIGNED)
+    assert st == moe.MOE_ERR_INVALID_ARG and "dw_router" in msg
+    st, msg = _bwd_call(BASE.replace(F_shared=64))
+    assert st == moe.MOE_ERR_INVALID_ARG and "dws13 is NULL" in msg
+    need_f = moe.workspace_size(BASE, moe.MOE_WS_LAYER)
+    st, msg = _bwd_call(BASE, fwd_bytes=need_f - 1)
+    assert st == moe.MOE_ERR_WORKSPACE and f"required ({need_f})" in msg
+    need_b = moe.workspace_size(BASE, moe.MOE_WS_LAYER_BWD)
+    st, msg = _bwd_call(BASE, ws_bytes=need_b - 1)
+    assert st == moe.MOE_ERR_WORKSPACE and f"required ({need_b})" in msg
+    st, msg = _bwd_call(BASE.replace(gate=wl.GATE_SIGMOID), bias=FAKE)
+    assert st == moe.MOE_ERR_UNSUPPORTED and "bias" in msg
