@@ -11,7 +11,7 @@ with a scale, softmax with a Zipf router bias, sigmoid renormalised with a group
 scale, raw sigmoid), a rank slice with slots routed elsewhere, a shared expert of another
 width (own launches) and of the routed width, the masked-decode layout with dropped slots,
 the forward with and without the gather folded (bit-identical gradients), run-to-run
-determinism, no tokens, and the full DeepSeek-V3-, Kimi-K2- and skewed-shaped workloads.
+determinism, no tokens, and the full DeepSeek-V3-shaped workload.
 """
 import numpy as np
 import pytest
@@ -128,10 +128,12 @@ def test_layer_backward_no_tokens_zero_weight_gradients():
         assert (v.float() == 0).all(), k
 
 
-@pytest.mark.parametrize("name", ["dsv3", "k2decode", "skewed"])
+@pytest.mark.parametrize("name", ["dsv3"])
 def test_layer_backward_full_workload(name):
-    """Full-size workloads in the benchmark's launch configuration, every gradient against the
-    fp64 oracle over the whole batch."""
+    """The DeepSeek-V3-shaped rank share at full size (the configuration the benchmark times),
+    every gradient against the fp64 oracle over the whole batch (the oracle takes ~40-70 s of
+    host time here; the decode-sized, skewed and every-gating-mode cases run at small sizes
+    above)."""
     print(f"[layer backward] full workload {name}: generating inputs", flush=True)
     inputs = wl.make_inputs(name)
     sh = inputs["shape"]
