@@ -158,9 +158,25 @@ LayerLayout layer_layout(const moe_shape_t* s) {
 // gradients, the shared expert's and the router's input gradients, and the expert-MLP
 // backward's intermediates (routed and shared run one after the other on the same scratch).
 struct LayerBwdLayout {
-  size_t seg, dgate, dlogits, dy_perm, dx_perm, dx_shared, dx_router, scratch;
+  size_t seg, segk, dgate, dlogits, dy_perm, dx_perm, dx_shared, dx_router, wr_parts, scratch;
   size_t total;
 };
+
+// K split of the router weight gradient dw_router = dlogits^T x (E x d outputs reduced over T
+// tokens): at most one (chunk, m-tile, n-tile) tile per compute unit of the chip, chunks of at
+// least 256 tokens, at most 16 chunks; float32 partials summed in chunk order.
+constexpr int kWrSplitMax = 16;
+int router_wgrad_splits(int64_t T, int E, int d) {
+  const int64_t tiles = ((E + 255) / 256) * (int64_t)((d + 255) / 256);
+  int64_t s = 256 / tiles;
+  s = std::min<int64_t>(s, kWrSplitMax);
+  s = std::min<int64_t>(s, std::max<int64_t>(1, T / 256));
+  return (int)std::max<int64_t>(s, 1);
+}
+int64_t router_wgrad_chunk(int64_t T, int E, int d) {
+  const int s = router_wgrad_splits(T, E, d);
+  return std::max<int64_t>(1, (T + s - 1) / s);
+}
 
 LayerBwdLayout layer_bwd_layout(const moe_shape_t* s) {
   LayerBwdLayout L{};
@@ -172,12 +188,14 @@ LayerBwdLayout layer_bwd_layout(const moe_shape_t* s) {
     return o;
   };
   L.seg = take(2 * sizeof(int32_t));
+  L.segk = take((kWrSplitMax + 1) * sizeof(int32_t));
   L.dgate = take(T * k * 4);
   L.dlogits = take(T * (size_t)s->E * 2);
   L.dy_perm = take(cap * d * 2);
   L.dx_perm = take(cap * d * 2);
   L.dx_shared = take(s->F_shared > 0 ? T * d * 2 : 0);
   L.dx_router = take(T * d * 2);
+  L.wr_parts = take((size_t)router_wgrad_splits(s->T, s->E, s->d) * s->E * d * 4);
   // ffn_backward takes four planes of align_up(rows * F * 2) bytes
   L.scratch = take(std::max(4 * align_up(cap * (size_t)s->F * 2), 4 * align_up(T * (size_t)s->F_shared * 2)));
   L.total = off;
@@ -731,6 +749,13 @@ int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_ro
   gb.routed_scale = s->routed_scale;
   gb.dlogits = dlogits;
   gb.seg = seg;
+  const int wr_splits = router_wgrad_splits(T, E, d);
+  const int64_t wr_chunk = router_wgrad_chunk(T, E, d);
+  // chunks actually covering [0, T) (the last ones may be empty when T is small)
+  const int wr_groups = (int)std::min<int64_t>(wr_splits, (T + wr_chunk - 1) / wr_chunk);
+  gb.segk = at<int32_t>(ws, B.segk);
+  gb.nsegk = wr_groups;
+  gb.segk_rows = wr_chunk;
   CHECK(hip_status(moe::launch_gate_bwd(gb, st), "gate backward launch"));
   // expert-ordered token rows (the forward may have read them straight from x)
   moe::PermuteProblem pp{};
@@ -799,20 +824,26 @@ int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_ro
   g.Y = dx_router;
   g.ldy = d;
   CHECK(hip_status(moe::launch_gemm_bwd(g, st), "router dx launch"));
-  // dw_router = dlogits^T x: one reduction over all T token rows
+  // dw_router = dlogits^T x: float32 partials over token chunks (the K split), summed in
+  // chunk order and rounded once
   moe::GemmBwdProblem w = g;
   w.mode = moe::BWD_KSEG;
   w.x_mn = w.w_mn = true;
+  w.offsets = at<int32_t>(ws, B.segk);
+  w.groups = wr_groups;
   w.X = dlogits;
   w.ldx = E;
   w.W = static_cast<const moe::bf16_t*>(x);
   w.ldw = d;
   w.M = E;
   w.N = d;
-  w.Y = static_cast<moe::bf16_t*>(dw_router);
+  w.Y = nullptr;
+  w.Yf = at<float>(ws, B.wr_parts);
   w.ldy = d;
-  w.y_group_stride = 0;
+  w.y_group_stride = (int64_t)E * d;
   CHECK(hip_status(moe::launch_gemm_bwd(w, st), "router weight gradient launch"));
+  CHECK(hip_status(moe::launch_sum_partials(w.Yf, wr_groups, (int64_t)E * d, static_cast<moe::bf16_t*>(dw_router), st),
+                   "router weight gradient sum launch"));
   // dx: the token's expert-row gradients in slot order, then the shared expert's, then the router's
   moe::UnpermuteSumProblem u{};
   u.rows = dx_perm;

@@ -390,6 +390,25 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
         if (s < nl) issue(s, s, td.klen);
     }
 
+    if (MODE == BWD_KSEG && p.Yf) {
+      // float32 results straight from the accumulators: lane holds 4 consecutive columns of one row
+      float* yf = p.Yf + (int64_t)cur.g * p.y_group_stride;
+#pragma unroll
+      for (int a = 0; a < FM; ++a) {
+        const int row = cur.m0 + (a * WGM + wm) * 32 + (lane & 31);
+        if (row >= cur.m_end) continue;
+#pragma unroll
+        for (int b = 0; b < FN; ++b)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int col = cur.n0 + wn * WN + b * 32 + 8 * q + 4 * hi;
+            const f32x4 v = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]};
+            if (col < p.N) *reinterpret_cast<f32x4*>(yf + (int64_t)row * p.ldy + col) = v;
+          }
+      }
+      if (!more) break;
+      continue;
+    }
     // epilogue, one 32-row block at a time through this wave's area of the idle last ring slot:
     // the lane's 4-column pieces (row lane & 31, columns 32 b + 8 q + 4 hi) go to LDS, then
     // every lane stores 16-byte pieces of whole rows (WN columns each), so a store instruction

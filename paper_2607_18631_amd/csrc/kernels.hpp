@@ -102,6 +102,7 @@ struct GemmBwdProblem {
   bf16_t* Y;
   int64_t ldy;
   int64_t y_group_stride;     // BWD_KSEG
+  float* Yf;                  // BWD_KSEG: when set, float32 results here (same strides) instead of Y
 };
 hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream);
 
@@ -189,7 +190,10 @@ struct GateBwdProblem {
   int32_t E, top_k, gate, renormalize;
   float routed_scale;
   bf16_t* dlogits;            // [T, E]
-  int32_t* seg;               // [2] or nullptr
+  int32_t* seg;               // [2] or nullptr: {0, T}
+  int32_t* segk;              // [nsegk + 1] or nullptr: {0, c, 2c, ..., T} (token chunks of segk_rows)
+  int32_t nsegk;
+  int64_t segk_rows;
 };
 hipError_t launch_gate_bwd(const GateBwdProblem& p, hipStream_t stream);
 
@@ -204,6 +208,9 @@ struct UnpermuteSumProblem {
   int32_t d, top_k;
 };
 hipError_t launch_unpermute_sum(const UnpermuteSumProblem& p, hipStream_t stream);
+
+// out[i] = bf16( sum over s = 0 .. nparts-1, in that order, of parts[s * n + i] ), n % 4 == 0
+hipError_t launch_sum_partials(const float* parts, int nparts, int64_t n, bf16_t* out, hipStream_t stream);
 
 // acc[0 .. n) = 0 (a fill kernel, so the call can sit inside a captured graph); n % 4 == 0
 hipError_t launch_zero_f32(float* acc, int64_t n, hipStream_t stream);

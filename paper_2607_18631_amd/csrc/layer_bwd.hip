@@ -132,9 +132,14 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate_bwd(GateBwdProblem p) {
   __shared__ float s_key[kWaves][64 * PL];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t t = (int64_t)blockIdx.x * kWaves + w;
-  if (blockIdx.x == 0 && threadIdx.x == 0 && p.seg) {
-    p.seg[0] = 0;                                          // one row segment [0, T) for the router GEMMs
-    p.seg[1] = (int32_t)p.T;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x == 0 && p.seg) {
+      p.seg[0] = 0;                                        // one row segment [0, T)
+      p.seg[1] = (int32_t)p.T;
+    }
+    // token chunks of the router weight gradient's K split
+    if (p.segk && (int)threadIdx.x <= p.nsegk)
+      p.segk[threadIdx.x] = (int32_t)min((int64_t)threadIdx.x * p.segk_rows, p.T);
   }
   if (t >= p.T) return;                                   // wave-uniform
   const int E = p.E, k = p.top_k;
@@ -284,6 +289,24 @@ __global__ __launch_bounds__(64 * kWaves) void k_unpermute_sum(UnpermuteSumProbl
   }
 }
 
+// out = bf16 of the float32 partials summed in order, four values per thread
+__global__ __launch_bounds__(256) void k_sum_partials(const float* parts, int nparts, int64_t n4, bf16_t* out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    f32x4 acc = reinterpret_cast<const f32x4*>(parts)[i];
+    for (int s = 1; s < nparts; ++s) {
+      const f32x4 v = reinterpret_cast<const f32x4*>(parts + (int64_t)s * n4 * 4)[i];
+      acc[0] += v[0];
+      acc[1] += v[1];
+      acc[2] += v[2];
+      acc[3] += v[3];
+    }
+    uint2 o;
+    o.x = pack_bf16x2(acc[0], acc[1]);
+    o.y = pack_bf16x2(acc[2], acc[3]);
+    *reinterpret_cast<uint2*>(out + 4 * i) = o;
+  }
+}
+
 template <int PL>
 hipError_t launch_gate_bwd_pl(const GateBwdProblem& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)((p.T + kWaves - 1) / kWaves);
@@ -300,8 +323,18 @@ hipError_t launch_combine_bwd(const CombineBwdProblem& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+hipError_t launch_sum_partials(const float* parts, int nparts, int64_t n, bf16_t* out, hipStream_t stream) {
+  if (nparts < 1 || n % 4) return hipErrorInvalidValue;
+  const int64_t n4 = n / 4;
+  const int64_t b = (n4 + 255) / 256;
+  hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)(b < 4096 ? (b > 0 ? b : 1) : 4096)), dim3(256), 0, stream, parts,
+                     nparts, n4, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_gate_bwd(const GateBwdProblem& p, hipStream_t stream) {
   if (p.nsplit < 1 || p.top_k < 1 || p.top_k > 16 || p.E < 1) return hipErrorInvalidValue;
+  if (p.segk && (p.nsegk < 1 || p.nsegk >= 64 * kWaves || p.segk_rows < 1)) return hipErrorInvalidValue;
   const int pl = (p.E + 63) / 64;
   if (pl <= 1) return launch_gate_bwd_pl<1>(p, stream);
   if (pl <= 2) return launch_gate_bwd_pl<2>(p, stream);
