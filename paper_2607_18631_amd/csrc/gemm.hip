@@ -435,6 +435,60 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
   }
 }
 
+// EPI_BF16 / EPI_SWIGLU through LDS: a lane's MFMA results are 4-column pieces of one row, so
+// storing them straight from registers writes 16-byte pieces of 32 rows per instruction.
+// Each 32-row block of the wave's sub-tile instead goes to a wave-private LDS area (`st`, 32 rows
+// of OUTW bf16) and comes back as 16-byte pieces of whole rows: a store instruction then writes
+// 64 / (OUTW / 8) full rows of OUTW columns.  The 16-byte piece c of staged row r sits at piece
+// c ^ (r % (OUTW / 8)), which spreads the 32 rows one write instruction touches over the banks.
+template <int EPI, int FM, int FN, int OUTW>
+__device__ __forceinline__ void store_tile_staged(const GemmProblem& p, const f32x16 (&acc)[FM][FN],
+                                                  const TileDesc& t, int trow, int astride, int fcol, int lane,
+                                                  bf16_t* st) {
+  static_assert(EPI == EPI_BF16 || EPI == EPI_SWIGLU, "staged epilogue: bf16 results");
+  constexpr int CPRW = OUTW / 8;                          // 16-byte pieces per staged row
+  constexpr int FO = EPI == EPI_SWIGLU ? FN / 2 : FN;     // output fragments per row block
+  static_assert(FO * 32 == OUTW && (32 * CPRW) % 64 == 0, "staged row width");
+  const int hi = lane >> 5, r = lane & 31;
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    const int rbase = t.row0 + trow + a * astride;       // first row of the 32-row block
+    if (rbase >= t.row_end) continue;                     // wave-uniform
+#pragma unroll
+    for (int b = 0; b < FO; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (EPI == EPI_SWIGLU) {
+            const float gt = acc[a][b][4 * q + e], up = acc[a][b + FN / 2][4 * q + e];
+            o[e] = gt / (1.0f + __expf(-gt)) * up;
+          } else {
+            o[e] = acc[a][b][4 * q + e];
+          }
+        }
+        uint2 v;
+        v.x = pack_bf16x2(o[0], o[1]);
+        v.y = pack_bf16x2(o[2], o[3]);
+        *reinterpret_cast<uint2*>(st + r * OUTW + (((b * 4 + q) ^ (r % CPRW)) << 3) + 4 * hi) = v;
+      }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int it = 0; it < 32 * CPRW / 64; ++it) {
+      const int idx = it * 64 + lane;
+      const int rr = idx / CPRW, c = idx % CPRW;
+      const int row = rbase + rr, col = fcol + c * 8;
+      const u32x4 v = ld16(st + rr * OUTW + ((c ^ (rr % CPRW)) << 3));
+      if (row < t.row_end && col < p.N)
+        st16(reinterpret_cast<bf16_t*>(t.Y) + (int64_t)row * p.ldy + col, v);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // EPI_SCATTER: the gate-weighted combine folded into the epilogue.  In the MFMA layout a lane
 // holds 4-column pieces of one token row, so adding the fragment straight from registers
 // would touch 32 rows (cache lines) per instruction; each 32 x 32 fragment instead goes
@@ -675,6 +729,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       static_assert(NW * 32 * kScatterLd * 4 <= SLICE * 2, "scatter staging fits one ring slot");
       float* lw = reinterpret_cast<float*>(ring + (STAGES - 1) * SLICE) + wave * 32 * kScatterLd;
       scatter_tile<FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane, lw);
+    } else if constexpr ((EPI == EPI_BF16 || EPI == EPI_SWIGLU) &&
+                         NW * 32 * (EPI == EPI_SWIGLU ? WN / 2 : WN) <= SLICE) {
+      // whole-row stores staged through the last ring slot (idle until the next tile's first barrier)
+      constexpr int OUTW = EPI == EPI_SWIGLU ? WN / 2 : WN;
+      bf16_t* st = ring + (STAGES - 1) * SLICE + wave * 32 * OUTW;
+      store_tile_staged<EPI, FM, FN, OUTW>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane, st);
     } else {
       store_tile<EPI, FM, FN>(p, acc, cur_td, wm * 32, WGM * 32, cur_td.ni * OUTN + fcol, lane);
     }

@@ -142,3 +142,43 @@ def test_layer_backward_full_workload(name):
     print(f"[layer backward] {name}: GPU backward ran, oracle on {sh.T} tokens", flush=True)
     ref, near = _oracle(inputs, layer, dout)
     _compare(name, got, ref)
+
+
+@pytest.mark.parametrize("capacity", [0, 6])
+def test_forward_backward_graph_replay(capacity):
+    """Forward and backward captured together in one HIP graph (the library issues no memset,
+    allocation or host synchronisation): three replays on new token rows and output gradients,
+    with eager calls and synchronisations between them, every gradient of every replay
+    bit-identical to the eager forward + backward on the same inputs."""
+    sh = S(T=64, d=512, E=32, top_k=4, F=256, E_local=8, F_shared=256, expert_capacity=capacity)
+    inputs = wl.custom_inputs(sh, seed=4, router_std=2 * 512 ** -0.5, zipf_s=1.1)
+    graphed = moe.DeviceLayer(inputs)
+    eager = moe.DeviceLayer(inputs)
+    dout = moe.to_device_bf16(_dout(sh, 1))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        graphed.forward()                                         # warm-up (allocates the workspaces)
+        graphed.backward(dout)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        graphed.forward()
+        grads = graphed.backward(dout)
+    rng = np.random.default_rng(98)
+    for rep in range(3):
+        xt = moe.to_device_bf16(wl.f32_to_bf16_bits(rng.standard_normal((sh.T, sh.d)).astype(np.float32)))
+        dt = moe.to_device_bf16(wl.f32_to_bf16_bits(rng.standard_normal((sh.T, sh.d)).astype(np.float32)))
+        graphed.x.copy_(xt)
+        dout.copy_(dt)
+        g.replay()
+        torch.cuda.synchronize()
+        got = {k: dev_bits(v) for k, v in grads.items() if v is not None}
+        eager.x.copy_(xt)
+        eager.forward()
+        want = {k: dev_bits(v) for k, v in eager.backward(dt).items() if v is not None}
+        torch.cuda.synchronize()
+        print(f"[graph] capacity={capacity} replay {rep}: checked", flush=True)
+        for k in want:
+            np.testing.assert_array_equal(got[k], want[k], err_msg=k)
