@@ -152,9 +152,7 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
   }
   if (tid == 0) s_tp[groups] = total_r;
   __syncthreads();
-  // the extra group's tiles are spread evenly among the grouped ones (position t is an extra
-  // tile iff floor((t+1) S / total) > floor(t S / total)), so HBM-bound expert tiles and
-  // compute-bound shared-expert tiles run side by side
+  // the extra group's tiles sit among the grouped ones (see extra_position)
   ts.tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * ts.tiles_n : 0;
   ts.base_total = total_r + ts.tiles_x;
   ts.nk = (p.K + BK - 1) / BK;
@@ -181,6 +179,37 @@ struct TileDesc {
   void* Y;
 };
 
+#ifndef MOE_EXTRA_BLOCKS
+#define MOE_EXTRA_BLOCKS 1
+#endif
+// Where the extra group's (shared expert's) tiles sit among the grouped ones: x_before = extra
+// tiles before position t, extra = position t is one.  Workgroup i runs on XCD i % 8 and an XCD
+// takes G / 8 consecutive positions per round of the persistent grid, so the extra tiles are
+// spread over whole such blocks: every block is all-extra or all-grouped (the last extra block
+// may be part-filled, its other positions grouped), which keeps the tiles an XCD runs together
+// on shared token and weight panels, while HBM-bound expert blocks and compute-bound shared
+// blocks still run side by side on the chip.  Problems with fewer full blocks than extra blocks
+// (or grids that are not whole rounds of the 8 XCDs) spread tile by tile.
+__device__ __forceinline__ void extra_position(const TileSpace& ts, int t, int& x_before, bool& extra) {
+  const int S = ts.tiles_x, T = ts.base_total;
+  const int G = gridDim.x;
+  const int BS = (MOE_EXTRA_BLOCKS && G % 8 == 0) ? G / 8 : 1;
+  const int nbf = T / BS;                                 // full blocks
+  const int sb = (S + BS - 1) / BS;                       // blocks the extra tiles fill
+  if (S == 0 || BS == 1 || sb > nbf) {
+    x_before = (int)((int64_t)t * S / T);
+    extra = (int)((int64_t)(t + 1) * S / T) > x_before;
+    return;
+  }
+  const int b = t / BS, o = t - b * BS;
+  // extra blocks among the full ones: block b is one iff floor((b+1) sb / nbf) > floor(b sb / nbf)
+  const int before = (int)((int64_t)min(b, nbf) * sb / nbf);
+  const bool xblock = b < nbf && (int)((int64_t)(b + 1) * sb / nbf) > before;
+  const int first = before * BS;                          // extra tiles in earlier blocks
+  extra = xblock && first + o < S;
+  x_before = min(S, first + (xblock ? o : 0));
+}
+
 template <int BM>
 __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const TileSpace& ts, int tile) {
   TileDesc d;
@@ -188,8 +217,9 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
   tile -= d.kc * ts.base_total;
   d.kb = d.kc * ts.kchunk;
   d.ke = min(ts.nk, d.kb + ts.kchunk);
-  const int x_before = (int)((int64_t)tile * ts.tiles_x / ts.base_total);
-  const bool extra = (int)((int64_t)(tile + 1) * ts.tiles_x / ts.base_total) > x_before;
+  int x_before;
+  bool extra;
+  extra_position(ts, tile, x_before, extra);
   int row0g, local;
   if (extra) {
     row0g = 0;
