@@ -324,6 +324,59 @@ def layer_backward_run(workload, steps):
                 "forward_tflops": fwd_flops / (t_fwd * 1e-3) / 1e12}
 
 
+def all_workloads_run(steps):
+    """Every workload of the metric's configuration list: per-call layer time (warmup 10, median of
+    3 round medians of `steps` calls), the per-step split from traced calls, tokens/s, the grouped
+    GEMMs' TFLOP/s, the layer's algorithmic HBM bytes per second, and the layer's roofline floor
+    max(FLOPs / bf16 peak, bytes / HBM peak) as a fraction of the measured time."""
+    import numpy as np
+    import torch
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    ev = HipEvents()
+    nstep = len(moe.MOE_STEP_NAMES)
+    rows = []
+    for name in wl.WORKLOADS:
+        log(f"workload {name}: generating inputs")
+        inputs = wl.make_inputs(name)
+        sh = inputs["shape"]
+        layer = moe.DeviceLayer(inputs, device="cuda:0")
+        t = timed_median(layer.forward, steps)
+        events = [ev.create(nstep + 1) for _ in range(steps)]
+        for i in range(steps):
+            layer.forward_traced(events[i])
+        torch.cuda.synchronize()
+        split = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in events]).mean(axis=0)
+        for e in events:
+            ev.destroy(e)
+        offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
+        n_loc = int(offsets[-1])
+        active = int((np.diff(offsets) > 0).sum())
+        d, F, Fs, T, k, E = sh.d, sh.F, sh.F_shared, sh.T, sh.top_k, sh.E
+        gemm_flops = 6.0 * d * F * n_loc + 6.0 * d * Fs * T
+        layer_flops = gemm_flops + 2.0 * T * d * E
+        layer_bytes = (active * 3 * d * F * 2 + 3 * d * Fs * 2 + E * d * 2 + 2 * T * d * 2 + T * k * 8)
+        s = {n: i for i, n in enumerate(moe.MOE_STEP_NAMES)}
+        gemm_ms = sum(split[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
+        floor_ms = max(layer_flops / (PEAK_BF16_TFLOPS * 1e12), layer_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+        bound = "mfma" if layer_flops / (PEAK_BF16_TFLOPS * 1e12) >= layer_bytes / (PEAK_HBM_GBS * 1e9) else "hbm"
+        rows.append({"workload": name, "T": T, "d": d, "E": E, "top_k": k, "E_local": sh.E_local, "F": F,
+                     "F_shared": Fs, "local_rows": n_loc, "active_local_experts": active,
+                     "layer_us": t * 1e3, "tokens_per_s": T / (t * 1e-3),
+                     "gemm_us": float(gemm_ms * 1e3), "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
+                     "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                     "layer_hbm_gbs": layer_bytes / (t * 1e-3) / 1e9,
+                     "layer_bound": bound, "layer_floor_us": floor_ms * 1e3,
+                     "layer_frac_of_roofline": floor_ms / t,
+                     "step_us": {n: round(float(split[i]) * 1e3, 2) for n, i in s.items()}})
+        log(f"{name}: {t * 1e3:.1f} us per layer, {rows[-1]['tokens_per_s']:.3g} tokens/s, "
+            f"GEMM {rows[-1]['gemm_tflops']:.0f} TFLOP/s, {rows[-1]['layer_hbm_gbs']:.0f} GB/s")
+        del layer, inputs
+        torch.cuda.empty_cache()
+    return rows
+
+
 def cpu_baseline(inputs, sample_tokens):
     """fp64 oracle (as it stands) on the first `sample_tokens` tokens: routing + expert MLPs + combine."""
     import numpy as np
@@ -366,6 +419,8 @@ def main():
                     help="time the layer of --workload in the four fuse_gather x fuse_combine structures")
     ap.add_argument("--backward", action="store_true",
                     help="time the expert-MLP backward on one routed batch of --workload")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="time the layer on every workload (tiny, mixtral, dsv3, skewed, k2decode)")
     ap.add_argument("--layer-backward", action="store_true",
                     help="time the whole layer backward (moe_layer_backward) of --workload")
     ap.add_argument("--capacity", type=int, default=0,
@@ -419,6 +474,17 @@ def main():
                                      "E_local": sh.E_local, "F": sh.F},
                           "protocol": "warmup 10; median of 3 round medians of the per-call event times",
                           **row}), flush=True)
+        return
+    if args.all_workloads:
+        rows = all_workloads_run(max(args.steps, 10))
+        print(json.dumps({"metric": "MoE-layer tokens/s, grouped-GEMM TFLOP/s and layer HBM GB/s per workload, "
+                                    "1 MI355X",
+                          "unit": "tokens/s", "higher_is_better": True, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic", "vs_baseline": None,
+                          "protocol": "warmup 10; median of 3 round medians of the per-call event times; step "
+                                      "split from traced calls",
+                          "peaks": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS},
+                          "rows": rows}), flush=True)
         return
     if args.layer_backward:
         sh, row = layer_backward_run(args.workload, max(args.steps, 10))
