@@ -1,5 +1,6 @@
 /*
- * moe.h -- C ABI of the MI355X (gfx950) MoE-layer forward library (libmoe_mi355x.so).
+ * moe.h -- C ABI of the MI355X (gfx950) MoE-layer library (libmoe_mi355x.so): the forward
+ * of one MoE layer and its backward.
  *
  * The library computes the forward pass of one Mixture-of-Experts layer on one
  * expert-parallel rank's share of the work: router logits, top-k gating, the
@@ -10,7 +11,9 @@
  * kernel-generation design (Section 3.1, kernel sub-plan: permute before the
  * grouped GEMM, weighted combine after it; Section 4, kernel generation: the
  * monotone [E+1] row-offset array; Section 4, engine registration: the forward
- * composes the expert MLP's two GEMMs).
+ * composes the expert MLP's two GEMMs).  The training leg's backward of the expert MLP and
+ * of the whole layer (moe_grouped_ffn_backward, moe_layer_backward) reuses the forward's
+ * routing and permutation.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
