@@ -51,30 +51,53 @@
 
 namespace moe {
 
-// device properties, queried once per device
+// device properties, queried once per device (concurrent first queries store the same values)
 struct DevInfo {
-  int cus = 0;
-  int lds = 0;
+  std::atomic<int> cus{0};
+  std::atomic<int> lds{0};
 };
-static DevInfo g_dev[64];
+static DevInfo g_dev[kMaxDevices];
 
-static DevInfo& dev_info() {
-  static DevInfo fallback{256, 65536};
+static DevInfo* dev_info() {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fallback;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
   DevInfo& d = g_dev[dev];
-  if (d.cus == 0) {
+  if (d.cus.load(std::memory_order_relaxed) == 0) {
     int n = 0, l = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
     if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || l <= 0)
       l = 65536;
-    d.lds = l;
-    d.cus = n;
+    d.lds.store(l, std::memory_order_relaxed);
+    d.cus.store(n, std::memory_order_relaxed);
   }
-  return d;
+  return &d;
 }
-int cu_count() { return dev_info().cus; }
-int lds_limit() { return dev_info().lds; }
+int cu_count() {
+  const DevInfo* d = dev_info();
+  return d ? d->cus.load(std::memory_order_relaxed) : 256;
+}
+int lds_limit() {
+  const DevInfo* d = dev_info();
+  return d ? d->lds.load(std::memory_order_relaxed) : 65536;
+}
+
+int kernel_occupancy(OccCache& c, const void* fn, int nth, size_t lds, hipError_t& err) {
+  err = hipSuccess;
+  int dev = 0;
+  if ((err = hipGetDevice(&dev)) != hipSuccess) return 0;
+  if (dev < 0 || dev >= kMaxDevices) {
+    err = hipErrorInvalidDevice;
+    return 0;
+  }
+  int v = c.per_cu[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  if ((err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess) return 0;
+  int occ = 0;
+  if ((err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, nth, lds)) != hipSuccess) return 0;
+  v = occ > 0 ? occ : 1;
+  c.per_cu[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
 
 namespace {
 
@@ -775,20 +798,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
 
 // Persistent launch of kernel `fn` (nth threads, lds bytes of dynamic LDS): grid = the
 // smaller of an upper bound of the launch's tile count and the resident workgroups, rounded
-// down to whole rounds of the 8 XCDs.  per_cu caches the kernel's occupancy (idempotent;
-// racing writers store the same value).
-hipError_t launch_persistent(const void* fn, int& per_cu, int nth, size_t lds, int bm, int outn,
+// down to whole rounds of the 8 XCDs.  `occ` caches the kernel's occupancy per device.
+hipError_t launch_persistent(const void* fn, OccCache& occ, int nth, size_t lds, int bm, int outn,
                              const GemmProblem& p, hipStream_t stream) {
   const size_t lds_static = 2 * (kMaxGroups + 1) * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
-  if (per_cu == 0) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    int occ = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, nth, lds);
-    if (e != hipSuccess) return e;
-    per_cu = occ > 0 ? occ : 1;
-  }
+  hipError_t err;
+  const int per_cu = kernel_occupancy(occ, fn, nth, lds, err);
+  if (err != hipSuccess) return err;
   const int64_t tiles_n = (p.N + outn - 1) / outn;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
@@ -806,9 +823,9 @@ hipError_t launch_persistent(const void* fn, int& per_cu, int nth, size_t lds, i
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int EPI, bool KTAIL>
 hipError_t launch_kernel(const GemmProblem& p, hipStream_t stream) {
-  static int per_cu = 0;
+  static OccCache occ;
   const void* fn = reinterpret_cast<const void*>(&k_grouped_gemm<BM, BN, BK, STAGES, WGM, WGN, EPI, KTAIL>);
-  return launch_persistent(fn, per_cu, 64 * WGM * WGN, (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t), BM,
+  return launch_persistent(fn, occ, 64 * WGM * WGN, (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t), BM,
                            swiglu_pairs(EPI) ? BN / 2 : BN, p, stream);
 }
 

@@ -458,19 +458,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC = 1>
 hipError_t launch_bwd(const GemmBwdProblem& p, hipStream_t stream) {
-  static int per_cu = 0;
+  static OccCache occ;
   const void* fn = reinterpret_cast<const void*>(&k_gemm_bwd<BM, BN, BK, STAGES, WGM, WGN, XMN, WMN, MODE, OCC>);
   const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_static = (MODE == BWD_ROWS ? 3 : 2) * (kMaxGroups + 1) * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
-  if (per_cu == 0) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    int occ = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64 * WGM * WGN, lds);
-    if (e != hipSuccess) return e;
-    per_cu = occ > 0 ? occ : 1;
-  }
+  hipError_t err;
+  const int per_cu = kernel_occupancy(occ, fn, 64 * WGM * WGN, lds, err);
+  if (err != hipSuccess) return err;
   const int64_t tn = (p.N + BN - 1) / BN;
   const int64_t upper = MODE == BWD_ROWS ? tn * ((p.max_rows + BM - 1) / BM + p.groups)
                                          : (int64_t)p.groups * ((p.M + BM - 1) / BM) * tn;

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace moe {
 
 typedef uint16_t bf16_t;
@@ -68,9 +70,18 @@ struct GemmProblem {
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
 
-// compute units and the LDS bytes per workgroup of the current device (queried once)
+// compute units and the LDS bytes per workgroup of the current device (queried once per device)
 int cu_count();
 int lds_limit();
+
+// Resident workgroups per CU of one kernel, cached per device: the first launch on a device
+// raises the kernel's dynamic-LDS limit to `lds` and queries the occupancy.  Concurrent first
+// launches compute and store the same value.  Returns 0 and sets err on failure.
+constexpr int kMaxDevices = 64;
+struct OccCache {
+  std::atomic<int> per_cu[kMaxDevices];
+};
+int kernel_occupancy(OccCache& c, const void* fn, int nth, size_t lds, hipError_t& err);
 
 // Grouped GEMMs of the expert-MLP backward:  Y[m, n] = sum_k X[m, k] * W[n, k]  with each
 // operand either K-major (element (r, k) at base + r * ld + k) or MN-major (element (k, r) at
