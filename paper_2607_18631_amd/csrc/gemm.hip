@@ -43,6 +43,7 @@
 // token rows (the permute folded into the prologue: row r of the tile is X row
 // row_index[r]); and the scatter epilogue (the weighted combine folded into the epilogue:
 // rows added, times their gate, into float32 token rows with atomics).
+#include <cmath>
 #include <type_traits>
 
 #include "common.hpp"
@@ -927,6 +928,22 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   const bool small_extra = p.rows2 <= 512;
   const int tier = (p.rows_hint > 0 && small_extra) ? (p.rows_hint <= 128 ? 20 : p.rows_hint <= 512 ? 5 : 6) : 6;
   int cfg_swiglu = tier, cfg_bf16 = tier;
+  // The down-projection's 256 x 256 tiles can leave most of the persistent grid's last round idle
+  // (Mixtral-shaped: ~36 m-tiles x 16 n-tiles on 256 CUs, 2.25 rounds); 256 x 128 tiles (twice
+  // the count) are used when they fill the rounds clearly better (Mixtral down-projection
+  // 1169-1183 -> 1097 us; the skewed workload, whose 256 x 256 rounds are full, stays)
+  if (tier == 6 && p.epi == EPI_BF16 && p.rows_hint > 0) {
+    const double cus = cu_count();
+    const int64_t groups = p.offsets ? p.groups : 1;
+    const double mt = (double)((p.rows_hint * groups + 255) / 256) + (groups > 1 ? groups / 2 : 0) +
+                      (double)((p.rows2 + 255) / 256);
+    auto fill = [&](double tiles) {
+      const double r = tiles / cus;
+      return r / std::ceil(r);
+    };
+    const double f256 = fill(mt * ((p.N + 255) / 256)), f128 = fill(mt * ((p.N + 127) / 128));
+    if (f256 < 0.85 && f128 > f256 + 0.1) cfg_bf16 = 7;
+  }
 #ifdef MOE_GEMM_SWEEP
   if (g_force_cfg[EPI_SWIGLU] >= 0) cfg_swiglu = g_force_cfg[EPI_SWIGLU];
   if (g_force_cfg[EPI_BF16] >= 0) cfg_bf16 = g_force_cfg[EPI_BF16];
