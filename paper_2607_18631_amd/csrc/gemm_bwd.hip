@@ -112,7 +112,7 @@ struct OpCopy {
         if constexpr (MN) o -= (uint32_t)(max(k0 + kr - (klen - 1), 0) * ld2);
         else o -= (uint32_t)(max(k0 + kr - (klen - 8), 0) * 2);
       }
-      dma16(reinterpret_cast<const bf16_t*>(sb + o), dst + (wave + NW * j) * 512);
+      dma16_sv(sb, o, dst + (wave + NW * j) * 512);
     }
   }
 
@@ -317,13 +317,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
       lds_barrier();
     }
   };
-  constexpr int NR = FM * (XMN ? 2 : 1) + FN * (WMN ? 2 : 1);   // LDS reads per K-step
   bf16x8 fx[2][FM], fw[2][FN];
-  int na_cur = FM;                                       // live token fragments of the current tile
-  auto load_frags = [&](int buf, const bf16_t* xs, int ks) {
+  // the first NA token fragments (the live ones) and every weight fragment of K-step ks
+  auto load_frags = [&](auto na, int buf, const bf16_t* xs, int ks) {
+    constexpr int NA = decltype(na)::value;
 #pragma unroll
-    for (int a = 0; a < FM; ++a)
-      if (a < na_cur) fx[buf][a] = frag_x(xs, a, ks);
+    for (int a = 0; a < NA; ++a) fx[buf][a] = frag_x(xs, a, ks);
 #pragma unroll
     for (int b = 0; b < FN; ++b) fw[buf][b] = frag_w(xs + BM * BK, b, ks);
   };
@@ -344,20 +343,20 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
       constexpr int NA = decltype(na)::value;
       if (nl == 0) return;
       sync_slice(0);
-      if constexpr (NA > 0) load_frags(0, ring, 0);
+      if constexpr (NA > 0) load_frags(na, 0, ring, 0);
       for (int i = 0; i < nl; ++i) {
         const bf16_t* xs = ring + (i % STAGES) * SLICE;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int cur = ks & 1;
           if (ks + 1 < KS) {
-            if constexpr (NA > 0) load_frags(cur ^ 1, xs, ks + 1);
+            if constexpr (NA > 0) load_frags(na, cur ^ 1, xs, ks + 1);
           } else {
             // this step's operands are in registers: publish the next slice now, so the barrier
             // and its first reads overlap this step's MFMAs (after the last slice the reads hit
             // a stale slot, harmlessly)
             sync_slice(i + 1);
-            if constexpr (NA > 0) load_frags(cur ^ 1, ring + ((i + 1) % STAGES) * SLICE, 0);
+            if constexpr (NA > 0) load_frags(na, cur ^ 1, ring + ((i + 1) % STAGES) * SLICE, 0);
           }
           if constexpr (NA > 0) {
 #pragma unroll
@@ -365,15 +364,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
 #pragma unroll
               for (int b = 0; b < FN; ++b)
                 acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
-            sched_step<NR, NA * FN>();
+            sched_step<NA * (XMN ? 2 : 1) + FN * (WMN ? 2 : 1), NA * FN>();
           }
         }
       }
     };
     const int live_blocks = min(BM / 32, (td.m_end - td.m0 + 31) / 32);
     const int na = __builtin_amdgcn_readfirstlane(max(0, (live_blocks - wm + WGM - 1) / WGM));
-    na_cur = na;
-    with_count<FM>(na, k_loop);
+    // weight-gradient tiles are full except at the edge of M: every block is computed there (the
+    // dead rows are clamped copies and are not stored), which leaves one K loop in the kernel
+    if constexpr (MODE == BWD_KSEG) k_loop(std::integral_constant<int, FM>{});
+    else with_count<FM>(na, k_loop);
 
     // next tile's first slice goes into slot 0 once every wave is done reading the ring
     const BTile cur = td;

@@ -22,6 +22,22 @@ __device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
   __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
 }
 
+// The same copy written as inline assembly, from a wave-uniform base `sbase` plus the lane's
+// 32-bit byte offset `voff`.  For kernels that read LDS with ds_read_b64_tr_b16: the compiler
+// makes every such read wait for all direct-to-LDS copies it knows of (vmcnt(0)), which would
+// serialise each slice's copies with the next slice's MFMAs.  Copies issued this way are
+// invisible to it; the kernel orders them itself (explicit vmcnt counts and barriers).  M0
+// carries the LDS address; kernels using this helper issue no compiler-generated LDS copies,
+// so nothing else of theirs keeps a value in M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16_sv(const char* sbase, uint32_t voff, bf16_t* dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)(dst);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 template <int BK>
 struct Swz {
   static constexpr int CPR = BK / 8;            // 16-byte chunks per row
