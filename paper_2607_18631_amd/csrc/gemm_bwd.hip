@@ -31,6 +31,7 @@
 // Persistent workgroups walk the tile list; the next tile's first slice is in flight during
 // the epilogue.  K tails (segments of any length) are fetched from clamped addresses and
 // zeroed in LDS; rows / columns past the edges are clamped and never stored.
+#include <cmath>
 #include <type_traits>
 
 #include "common.hpp"
@@ -491,7 +492,27 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
     if (p.x_mn || !p.w_mn || p.K < 8 || p.K % 8) return hipErrorInvalidValue;
     if (p.rows_hint > 0 && p.rows_hint <= 128)
       return launch_bwd<64, 128, 64, 3, 2, 2, false, true, BWD_ROWS>(p, stream);
-    return launch_bwd<256, 256, 64, 2, 4, 2, false, true, BWD_ROWS>(p, stream);
+    // 256 x 256 tiles over 2 x 4 waves: a wave holds 128 token rows x 64 weight columns, so a
+    // K-step reads four token fragments (ds_read_b128) and two weight fragments (two
+    // ds_read_b64_tr_b16 each) for its 8 MFMAs; 4 x 2 waves read two and four, and the transpose
+    // reads are the dearer ones (DeepSeek-V3 routed dX 816 -> 634 us, shared dX 605 -> 481).
+    // 256 x 128 tiles (4 x 2 waves) when the 256 x 256 tile count leaves the persistent grid's
+    // last round mostly idle and the narrower tiles fill it clearly better (routed dA, 376
+    // tiles on 256 CUs: 409 -> 366 us).
+    const double cus = cu_count();
+    const double rows = p.rows_hint > 0 ? (double)p.rows_hint * p.groups : (double)p.max_rows;
+    const double mt = std::ceil(rows / 256.0) + (p.groups > 1 ? p.groups / 2 : 0);
+    auto fill = [&](double tiles) {
+      const double r = tiles / cus;
+      return r > 0 ? r / std::ceil(r) : 1.0;
+    };
+    const double f256 = fill(mt * ((p.N + 255) / 256)), f128 = fill(mt * ((p.N + 127) / 128));
+    int cfg = (f256 < 0.85 && f128 > f256 + 0.1) ? 2 : 1;
+#ifdef MOE_BWD_ROWS_CFG
+    cfg = MOE_BWD_ROWS_CFG;
+#endif
+    if (cfg == 2) return launch_bwd<256, 128, 64, 3, 4, 2, false, true, BWD_ROWS>(p, stream);
+    return launch_bwd<256, 256, 64, 2, 2, 4, false, true, BWD_ROWS>(p, stream);
   }
   if (p.mode == BWD_KSEG) {
     // weight gradients: both operands row-major activations reduced over the group's rows

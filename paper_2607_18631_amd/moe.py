@@ -55,6 +55,11 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it first (python -m paper_2607_18631_amd.build)")
+        # torch ships its own HIP runtime under the same soname (libamdhip64.so.7) as the system
+        # one the library is linked against.  Loading torch first makes the library bind to that
+        # runtime; loaded the other way round, the process holds two runtimes and the library's
+        # kernels are not found for torch's device memory ("invalid device function").
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         sp = ctypes.POINTER(MoEShapeC)
         L.moe_abi_version.restype = ctypes.c_int

@@ -285,3 +285,24 @@ def test_grouped_ffn_ragged_tail_blocks():
         ref = oracle.swiglu_ffn(xd[a:b], oracle.bf16_to_f64(w13[e]), oracle.bf16_to_f64(w2[e]))
         err = rel_fro(got[a:b], ref)
         assert err <= REL_TOL, (e, lengths[e], err)
+
+
+def test_library_loaded_before_torch():
+    """The binding loaded before anything imported torch (a fresh process) still runs the layer:
+    the library must bind to the HIP runtime torch uses, not to a second copy of it."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2607_18631_amd import moe\n"
+            "moe.lib()\n"
+            "import torch\n"
+            "from paper_2607_18631_amd import workloads as wl\n"
+            "layer = moe.DeviceLayer(wl.make_inputs('tiny'))\n"
+            "out = layer.forward()\n"
+            "torch.cuda.synchronize()\n"
+            "assert bool(torch.isfinite(out.float()).all())\n"
+            "print('ok')\n") % root
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout[-2000:] + r.stderr[-2000:]
