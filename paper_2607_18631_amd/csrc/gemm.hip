@@ -848,6 +848,7 @@ hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
     case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI>(p, stream);
     case 6: return launch_tile<256, 256, 64, 2, 4, 2, EPI>(p, stream);
     case 7: return launch_tile<256, 128, 64, 3, 4, 2, EPI>(p, stream);
+    case 8: return launch_tile<320, 256, 64, 2, 2, 4, EPI>(p, stream);
     // few rows per group (decode-like): 64 x 128 tiles, 4 waves, 3-slot ring, two workgroups per CU
     case 20: return launch_tile<64, 128, 64, 3, 2, 2, EPI>(p, stream);
 #ifdef MOE_GEMM_SWEEP
@@ -928,21 +929,43 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   const bool small_extra = p.rows2 <= 512;
   const int tier = (p.rows_hint > 0 && small_extra) ? (p.rows_hint <= 128 ? 20 : p.rows_hint <= 512 ? 5 : 6) : 6;
   int cfg_swiglu = tier, cfg_bf16 = tier;
-  // The down-projection's 256 x 256 tiles can leave most of the persistent grid's last round idle
-  // (Mixtral-shaped: ~36 m-tiles x 16 n-tiles on 256 CUs, 2.25 rounds); 256 x 128 tiles (twice
-  // the count) are used when they fill the rounds clearly better (Mixtral down-projection
-  // 1169-1183 -> 1097 us; the skewed workload, whose 256 x 256 rounds are full, stays)
-  if (tier == 6 && p.epi == EPI_BF16 && p.rows_hint > 0) {
+  // Tile shape for the MFMA-bound tier, from the expected tile count of each shape.  A persistent
+  // launch takes about ceil(tiles / CUs) rounds of its slowest workgroup; a 320 x 256 tile (10
+  // token blocks, 2 x 4 waves) costs ~1.15 rounds of a 256 x 256 one, a 256 x 128 tile ~0.6.  The
+  // per-expert row counts of a routed batch scatter around their mean (standard deviation about
+  // its square root), so an expert whose mean is 256 rows takes 1.5 256-row m-tiles on average but
+  // one 320-row tile: DeepSeek-V3 shapes (256 rows per expert, shared expert of 8192 rows in the
+  // launch) run both projections on 320-row tiles (up 1085-1093 -> 1000-1025 us, down 588-596 ->
+  // 565-568), Mixtral shapes (1024 rows per expert, 2.25 rounds of 256 x 256 down-projection
+  // tiles) their down-projection (1137-1147 -> 944-955; 256 x 128 tiles: 1097), while
+  // Mixtral's up-projection (15.75 rounds either way) and the skewed workload stay on 256 x 256.
+  if (tier == 6 && p.rows_hint > 0 && (p.epi == EPI_SWIGLU || p.epi == EPI_BF16)) {
     const double cus = cu_count();
     const int64_t groups = p.offsets ? p.groups : 1;
-    const double mt = (double)((p.rows_hint * groups + 255) / 256) + (groups > 1 ? groups / 2 : 0) +
-                      (double)((p.rows2 + 255) / 256);
-    auto fill = [&](double tiles) {
-      const double r = tiles / cus;
-      return r / std::ceil(r);
+    const double mu = (double)p.rows_hint;
+    const double sigma = groups > 1 ? std::sqrt(mu) : 0.0;
+    auto mtiles = [&](int bm) {                          // expected m-tiles of the launch
+      double per_group = 0;
+      if (sigma == 0) {
+        per_group = std::ceil(mu / bm);
+      } else {
+        const int jmax = (int)((mu + 8 * sigma) / bm) + 1;
+        for (int j = 0; j <= jmax; ++j)                   // E[ceil(m / bm)] = sum_j P(m > j bm)
+          per_group += 0.5 * std::erfc((j * bm - mu) / (sigma * std::sqrt(2.0)));
+      }
+      return per_group * groups + std::ceil((double)p.rows2 / bm);
     };
-    const double f256 = fill(mt * ((p.N + 255) / 256)), f128 = fill(mt * ((p.N + 127) / 128));
-    if (f256 < 0.85 && f128 > f256 + 0.1) cfg_bf16 = 7;
+    auto rounds = [&](double tiles) { return std::ceil(tiles / cus); };
+    const double tn = (double)((p.N + 127) / 128);        // 128-column output blocks
+    const double m256 = mtiles(256), m320 = mtiles(320);
+    if (p.epi == EPI_SWIGLU) {                            // a tile yields 128 output columns
+      if (1.15 * rounds(m320 * tn) < rounds(m256 * tn)) cfg_swiglu = 8;
+    } else {
+      const double tn256 = std::ceil(tn / 2);
+      const double c6 = rounds(m256 * tn256), c7 = 0.6 * rounds(m256 * tn), c8 = 1.15 * rounds(m320 * tn256);
+      if (c8 < c6 && c8 <= c7) cfg_bf16 = 8;
+      else if (c7 < c6) cfg_bf16 = 7;
+    }
   }
 #ifdef MOE_GEMM_SWEEP
   if (g_force_cfg[EPI_SWIGLU] >= 0) cfg_swiglu = g_force_cfg[EPI_SWIGLU];
