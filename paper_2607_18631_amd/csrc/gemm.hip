@@ -929,17 +929,20 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   const bool small_extra = p.rows2 <= 512;
   const int tier = (p.rows_hint > 0 && small_extra) ? (p.rows_hint <= 128 ? 20 : p.rows_hint <= 512 ? 5 : 6) : 6;
   int cfg_swiglu = tier, cfg_bf16 = tier;
-  // Tile shape for the MFMA-bound tier, from the expected tile count of each shape.  A persistent
-  // launch takes about ceil(tiles / CUs) rounds of its slowest workgroup; a 320 x 256 tile (10
-  // token blocks, 2 x 4 waves) costs ~1.15 rounds of a 256 x 256 one, a 256 x 128 tile ~0.6.  The
-  // per-expert row counts of a routed batch scatter around their mean (standard deviation about
-  // its square root), so an expert whose mean is 256 rows takes 1.5 256-row m-tiles on average but
-  // one 320-row tile: DeepSeek-V3 shapes (256 rows per expert, shared expert of 8192 rows in the
-  // launch) run both projections on 320-row tiles (up 1085-1093 -> 1000-1025 us, down 588-596 ->
-  // 565-568), Mixtral shapes (1024 rows per expert, 2.25 rounds of 256 x 256 down-projection
-  // tiles) their down-projection (1137-1147 -> 944-955; 256 x 128 tiles: 1097), while
-  // Mixtral's up-projection (15.75 rounds either way) and the skewed workload stay on 256 x 256.
-  if (tier == 6 && p.rows_hint > 0 && (p.epi == EPI_SWIGLU || p.epi == EPI_BF16)) {
+  // Tile shape from the expected tile count of each shape.  A persistent launch takes about
+  // ceil(tiles / CUs) rounds of its slowest workgroup; per tile, a 320 x 256 tile (10 token
+  // blocks, 2 x 4 waves) costs ~1.15 of a 256 x 256 one, a 128 x 256 tile ~0.7, a 256 x 128 tile
+  // ~0.6 (measured).  The per-expert row counts of a routed batch scatter around their mean
+  // (standard deviation about its square root), so an expert whose mean is 256 rows takes 1.5
+  // 256-row m-tiles on average but one 320-row tile: DeepSeek-V3 shapes (256 rows per expert,
+  // shared expert of 8192 rows in the launch) run both projections on 320-row tiles (up
+  // 1085-1093 -> 1000-1025 us, down 588-596 -> 565-568), Mixtral shapes (1024 rows per expert,
+  // 2.25 rounds of 256 x 256 down-projection tiles) their down-projection (1137-1147 -> 944-955;
+  // 256 x 128 tiles: 1097), while Mixtral's up-projection (15.75 rounds either way) and the
+  // skewed workload stay on 256 x 256.  The backward's recomputed up-projection of the routed
+  // experts alone (tier 128 x 256) takes 320-row tiles at DeepSeek-V3 (627 -> 521 us).
+  int cfg_swiglu_bwd = tier;
+  if ((tier == 5 || tier == 6) && p.rows_hint > 0) {
     const double cus = cu_count();
     const int64_t groups = p.offsets ? p.groups : 1;
     const double mu = (double)p.rows_hint;
@@ -957,12 +960,17 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
     };
     auto rounds = [&](double tiles) { return std::ceil(tiles / cus); };
     const double tn = (double)((p.N + 127) / 128);        // 128-column output blocks
-    const double m256 = mtiles(256), m320 = mtiles(320);
-    if (p.epi == EPI_SWIGLU) {                            // a tile yields 128 output columns
-      if (1.15 * rounds(m320 * tn) < rounds(m256 * tn)) cfg_swiglu = 8;
+    const double tn256 = std::ceil(tn / 2);
+    const double m128 = mtiles(128), m256 = mtiles(256), m320 = mtiles(320);
+    // SwiGLU epilogues: a 256-row weight tile yields 128 output columns
+    const double s_base = tier == 5 ? 0.7 * rounds(m128 * tn) : rounds(m256 * tn);
+    if (1.15 * rounds(m320 * tn) < s_base) cfg_swiglu = cfg_swiglu_bwd = 8;
+    // bf16 epilogue: also 256 x 128 tiles on the 256-row tier
+    const double c8 = 1.15 * rounds(m320 * tn256);
+    if (tier == 5) {
+      if (c8 < 0.7 * rounds(m128 * tn256)) cfg_bf16 = 8;
     } else {
-      const double tn256 = std::ceil(tn / 2);
-      const double c6 = rounds(m256 * tn256), c7 = 0.6 * rounds(m256 * tn), c8 = 1.15 * rounds(m320 * tn256);
+      const double c6 = rounds(m256 * tn256), c7 = 0.6 * rounds(m256 * tn);
       if (c8 < c6 && c8 <= c7) cfg_bf16 = 8;
       else if (c7 < c6) cfg_bf16 = 7;
     }
@@ -975,9 +983,10 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
     case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
     case EPI_SWIGLU_BWD:
       if (!p.dact || !p.act_out || p.rows2 > 0 || p.ldy != 2 * (int64_t)p.N) return hipErrorInvalidValue;
-      switch (tier) {      // the tiers of the forward up-projection (same operand shapes)
+      switch (cfg_swiglu_bwd) {      // the tiers of the forward up-projection (same operand shapes)
         case 20: return launch_tile<64, 128, 64, 3, 2, 2, EPI_SWIGLU_BWD>(p, stream);
         case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI_SWIGLU_BWD>(p, stream);
+        case 8: return launch_tile<320, 256, 64, 2, 2, 4, EPI_SWIGLU_BWD>(p, stream);
         default: return launch_tile<256, 256, 64, 2, 4, 2, EPI_SWIGLU_BWD>(p, stream);
       }
     case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
