@@ -99,11 +99,13 @@ struct OpCopy {
     else return (pc ^ Z::f(row)) * 8;
   }
 
-  // slice kt of a K range of klen into the LDS block dst (this wave's L instructions)
+  // slice kt of a K range of klen into the LDS block dst (this wave's L instructions); KT =
+  // false: klen is a multiple of BK (no tail slice, no tail code)
+  template <bool KT>
   __device__ __forceinline__ void issue(bf16_t* dst, int kt, int klen, int wave) const {
     const int lane = threadIdx.x & 63;
     const int k0 = kt * BK;
-    const bool tail = k0 + BK > klen;
+    const bool tail = KT && k0 + BK > klen;
     const char* sb = MN ? base + (int64_t)k0 * ld2 : base + k0 * 2;
 #pragma unroll
     for (int j = 0; j < L; ++j) {
@@ -130,7 +132,7 @@ struct OpCopy {
   }
 };
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC, bool KTAIL>
 __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem p) {
   constexpr int NW = WGM * WGN, NTH = 64 * NW;
   static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
@@ -243,8 +245,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
   };
   auto issue = [&](int kt, int slot, int klen) {
     bf16_t* dst = ring + slot * SLICE;
-    cx.issue(dst, kt, klen, wave);
-    cw.issue(dst + BM * BK, kt, klen, wave);
+    cx.template issue<KTAIL>(dst, kt, klen, wave);
+    cw.template issue<KTAIL>(dst + BM * BK, kt, klen, wave);
   };
 
   // per-lane LDS fragment offsets (elements), K-step 0
@@ -311,7 +313,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
     else wait_vmcnt<0>();
     lds_barrier();
     if (i + STAGES - 1 < nl) issue(i + STAGES - 1, (i + STAGES - 1) % STAGES, td.klen);
-    if (i < nl && (i + 1) * BK > td.klen) {
+    if (KTAIL && i < nl && (i + 1) * BK > td.klen) {
       bf16_t* xs = ring + (i % STAGES) * SLICE;
       CX::zero_tail(xs, i, td.klen, tid, NTH);
       CW::zero_tail(xs + BM * BK, i, td.klen, tid, NTH);
@@ -458,10 +460,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void k_gemm_bwd(GemmBwdProblem
   }
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC = 1>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool XMN, bool WMN, int MODE, int OCC = 1,
+          bool KTAIL = true>
 hipError_t launch_bwd(const GemmBwdProblem& p, hipStream_t stream) {
   static OccCache occ;
-  const void* fn = reinterpret_cast<const void*>(&k_gemm_bwd<BM, BN, BK, STAGES, WGM, WGN, XMN, WMN, MODE, OCC>);
+  if (!KTAIL && p.K % BK) return hipErrorInvalidValue;
+  const void* fn = reinterpret_cast<const void*>(&k_gemm_bwd<BM, BN, BK, STAGES, WGM, WGN, XMN, WMN, MODE, OCC, KTAIL>);
   const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_static = (MODE == BWD_ROWS ? 3 : 2) * (kMaxGroups + 1) * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
@@ -490,29 +494,50 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
   if (p.mode == BWD_ROWS) {
     // dA / dX: K-major activation rows against an MN-major weight
     if (p.x_mn || !p.w_mn || p.K < 8 || p.K % 8) return hipErrorInvalidValue;
+    // K a multiple of 64 (every expert and shared dimension of the measured workloads): the
+    // instances without K-tail code, which also leave the registers the 320-row tile needs
+    const bool kt = p.K % 64 != 0;
     if (p.rows_hint > 0 && p.rows_hint <= 128)
-      return launch_bwd<64, 128, 64, 3, 2, 2, false, true, BWD_ROWS>(p, stream);
-    // 256 x 256 tiles over 2 x 4 waves: a wave holds 128 token rows x 64 weight columns, so a
-    // K-step reads four token fragments (ds_read_b128) and two weight fragments (two
-    // ds_read_b64_tr_b16 each) for its 8 MFMAs; 4 x 2 waves read two and four, and the transpose
-    // reads are the dearer ones (DeepSeek-V3 routed dX 816 -> 634 us, shared dX 605 -> 481).
-    // 256 x 128 tiles (4 x 2 waves) when the 256 x 256 tile count leaves the persistent grid's
-    // last round mostly idle and the narrower tiles fill it clearly better (routed dA, 376
-    // tiles on 256 CUs: 409 -> 366 us).
+      return kt ? launch_bwd<64, 128, 64, 3, 2, 2, false, true, BWD_ROWS, 1, true>(p, stream)
+                : launch_bwd<64, 128, 64, 3, 2, 2, false, true, BWD_ROWS, 1, false>(p, stream);
+    // Tile shapes (all on the MN-major weight operand, two ds_read_b64_tr_b16 per fragment):
+    // 256 x 256 over 2 x 4 waves, a wave holding 128 token rows x 64 weight columns, so a K-step
+    // reads four token fragments (ds_read_b128) and two weight fragments, against two and four
+    // with 4 x 2 waves -- the transpose reads are the dearer ones (DeepSeek-V3 routed dX 816 ->
+    // 634 us, shared dX 605 -> 481); 256 x 128 (4 x 2 waves); 320 x 256 (2 x 4 waves, 10 token
+    // blocks).  Chosen like the forward's tiles, from the expected tile count of each shape: a
+    // persistent launch takes about ceil(tiles / CUs) rounds, a 256 x 128 tile costs ~0.6 of a
+    // 256 x 256 one and a 320-row tile ~1.15, and an expert's rows scatter around their mean with a
+    // standard deviation of about its square root (at 256 rows per expert: 1.5 256-row m-tiles on
+    // average, one 320-row tile).
     const double cus = cu_count();
-    const double rows = p.rows_hint > 0 ? (double)p.rows_hint * p.groups : (double)p.max_rows;
-    const double mt = std::ceil(rows / 256.0) + (p.groups > 1 ? p.groups / 2 : 0);
-    auto fill = [&](double tiles) {
-      const double r = tiles / cus;
-      return r > 0 ? r / std::ceil(r) : 1.0;
+    const double mu = p.rows_hint > 0 ? (double)p.rows_hint : (double)p.max_rows / p.groups;
+    const double sigma = p.groups > 1 ? std::sqrt(mu) : 0.0;
+    auto mtiles = [&](int bm) {
+      double per_group = 0;
+      if (sigma == 0) {
+        per_group = std::ceil(mu / bm);
+      } else {
+        const int jmax = (int)((mu + 8 * sigma) / bm) + 1;
+        for (int j = 0; j <= jmax; ++j)                   // E[ceil(m / bm)] = sum_j P(m > j bm)
+          per_group += 0.5 * std::erfc((j * bm - mu) / (sigma * std::sqrt(2.0)));
+      }
+      return per_group * p.groups;
     };
-    const double f256 = fill(mt * ((p.N + 255) / 256)), f128 = fill(mt * ((p.N + 127) / 128));
-    int cfg = (f256 < 0.85 && f128 > f256 + 0.1) ? 2 : 1;
+    auto rounds = [&](double tiles) { return std::ceil(tiles / cus); };
+    const double tn256 = (double)((p.N + 255) / 256), tn128 = (double)((p.N + 127) / 128);
+    const double c1 = rounds(mtiles(256) * tn256), c2 = 0.6 * rounds(mtiles(256) * tn128);
+    const double c3 = kt ? 1e30 : 1.15 * rounds(mtiles(320) * tn256);   // no tail instance of it
+    int cfg = (c3 < c1 && c3 <= c2) ? 3 : c2 < c1 ? 2 : 1;
 #ifdef MOE_BWD_ROWS_CFG
     cfg = MOE_BWD_ROWS_CFG;
 #endif
-    if (cfg == 2) return launch_bwd<256, 128, 64, 3, 4, 2, false, true, BWD_ROWS>(p, stream);
-    return launch_bwd<256, 256, 64, 2, 2, 4, false, true, BWD_ROWS>(p, stream);
+    if (cfg == 3 && !kt) return launch_bwd<320, 256, 64, 2, 2, 4, false, true, BWD_ROWS, 1, false>(p, stream);
+    if (cfg == 2)
+      return kt ? launch_bwd<256, 128, 64, 3, 4, 2, false, true, BWD_ROWS, 1, true>(p, stream)
+                : launch_bwd<256, 128, 64, 3, 4, 2, false, true, BWD_ROWS, 1, false>(p, stream);
+    return kt ? launch_bwd<256, 256, 64, 2, 2, 4, false, true, BWD_ROWS, 1, true>(p, stream)
+              : launch_bwd<256, 256, 64, 2, 2, 4, false, true, BWD_ROWS, 1, false>(p, stream);
   }
   if (p.mode == BWD_KSEG) {
     // weight gradients: both operands row-major activations reduced over the group's rows
