@@ -43,6 +43,7 @@
 // token rows (the permute folded into the prologue: row r of the tile is X row
 // row_index[r]); and the scatter epilogue (the weighted combine folded into the epilogue:
 // rows added, times their gate, into float32 token rows with atomics).
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -958,7 +959,9 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
       }
       return per_group * groups + std::ceil((double)p.rows2 / bm);
     };
-    auto rounds = [&](double tiles) { return std::ceil(tiles / cus); };
+    // rounds of the persistent grid; an expected count a few hundredths of a round above a
+    // whole number (the normal tail of the row counts) is that whole number
+    auto rounds = [&](double tiles) { return std::max(1.0, std::ceil(tiles / cus - 0.05)); };
     const double tn = (double)((p.N + 127) / 128);        // 128-column output blocks
     const double tn256 = std::ceil(tn / 2);
     const double m128 = mtiles(128), m256 = mtiles(256), m320 = mtiles(320);

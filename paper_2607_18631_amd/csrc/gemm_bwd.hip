@@ -31,6 +31,7 @@
 // Persistent workgroups walk the tile list; the next tile's first slice is in flight during
 // the epilogue.  K tails (segments of any length) are fetched from clamped addresses and
 // zeroed in LDS; rows / columns past the edges are clamped and never stored.
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -524,7 +525,9 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
       }
       return per_group * p.groups;
     };
-    auto rounds = [&](double tiles) { return std::ceil(tiles / cus); };
+    // rounds of the persistent grid; an expected count a few hundredths of a round above a
+    // whole number (the normal tail of the row counts) is that whole number
+    auto rounds = [&](double tiles) { return std::max(1.0, std::ceil(tiles / cus - 0.05)); };
     const double tn256 = (double)((p.N + 255) / 256), tn128 = (double)((p.N + 127) / 128);
     const double c1 = rounds(mtiles(256) * tn256), c2 = 0.6 * rounds(mtiles(256) * tn128);
     const double c3 = kt ? 1e30 : 1.15 * rounds(mtiles(320) * tn256);   // no tail instance of it

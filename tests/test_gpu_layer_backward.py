@@ -9,8 +9,8 @@ oracle uses the GPU's (equally valid) choice for that token (the routing protoco
 forward tests).  Cases: every gating mode (softmax renormalised, softmax over all experts
 with a scale, softmax with a Zipf router bias, sigmoid renormalised with a group limit and a
 scale, raw sigmoid), a rank slice with slots routed elsewhere, a shared expert of another
-width (own launches) and of the routed width, the masked-decode layout with dropped slots,
-the forward with and without the gather folded (bit-identical gradients), run-to-run
+width (own launches) and of the routed width, the masked-decode layout with dropped slots, a
+shape whose routed products take 320-row tiles, the forward with and without the gather folded (bit-identical gradients), run-to-run
 determinism, no tokens, and the full DeepSeek-V3-shaped workload.
 """
 import numpy as np
@@ -39,6 +39,9 @@ CASES = {
     "merged_shared_decode": (S(T=5, d=1024, E=96, top_k=8, F=256, E_local=12, F_shared=256,
                                gate=wl.GATE_SIGMOID), None, 0.0),
     "masked_drops": (S(T=120, d=192, E=16, top_k=4, F=64, E_local=16, expert_capacity=12, F_shared=64), None, 0.0),
+    # 256 rows per expert on average over 32 experts, d and 2F multiples of 64: the routed dX runs
+    # on the 320-row tile without K-tail code, the recomputed up-projection on 320-row tiles
+    "tile320_rows": (S(T=1024, d=2048, E=32, top_k=8, F=1024, E_local=32), None, 0.0),
 }
 GRADS = ("dx", "dw_router", "dw13", "dw2", "dws13", "dws2")
 

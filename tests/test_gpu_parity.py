@@ -36,6 +36,9 @@ SMALL = {
     "sigmoid_slice_end": (S(T=150, d=64, E=40, top_k=5, F=40, E_local=7, e_begin=33, gate=wl.GATE_SIGMOID,
                             renormalize=0), None, 0.0),
     "max_experts_top16": (S(T=70, d=64, E=1024, top_k=16, F=16, E_local=1024), None, 0.0),
+    # 256 rows per expert on average over 32 experts with K tails in both projections (d, F not
+    # multiples of 64): enough tiles that both projections take 320-row tiles, with tail slices
+    "tile320_ktail": (S(T=1024, d=2000, E=32, top_k=8, F=1000, E_local=32), None, 0.0),
     # the kernel-crossover shape at expert multiplicities 4 and 32
     "crossover_me4": (wl.crossover(4).shape, None, 0.0),
     "crossover_me32": (wl.crossover(32).shape, None, 0.0),
