@@ -841,11 +841,6 @@ hipError_t launch_tile(const GemmProblem& p, hipStream_t stream) {
 template <int EPI>
 hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
   switch (cfg) {
-    case 0: return launch_tile<128, 128, 64, 2, 2, 2, EPI>(p, stream);
-    case 1: return launch_tile<128, 256, 64, 3, 2, 2, EPI>(p, stream);
-    case 2: return launch_tile<256, 256, 64, 2, 2, 4, EPI>(p, stream);
-    case 3: return launch_tile<256, 256, 32, 4, 2, 4, EPI>(p, stream);
-    case 4: return launch_tile<128, 512, 32, 3, 2, 4, EPI>(p, stream);
     case 5: return launch_tile<128, 256, 64, 3, 2, 4, EPI>(p, stream);
     case 6: return launch_tile<256, 256, 64, 2, 4, 2, EPI>(p, stream);
     case 7: return launch_tile<256, 128, 64, 3, 4, 2, EPI>(p, stream);
@@ -853,6 +848,12 @@ hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
     // few rows per group (decode-like): 64 x 128 tiles, 4 waves, 3-slot ring, two workgroups per CU
     case 20: return launch_tile<64, 128, 64, 3, 2, 2, EPI>(p, stream);
 #ifdef MOE_GEMM_SWEEP
+    // tuning-sweep shapes (not chosen by the launcher)
+    case 0: return launch_tile<128, 128, 64, 2, 2, 2, EPI>(p, stream);
+    case 1: return launch_tile<128, 256, 64, 3, 2, 2, EPI>(p, stream);
+    case 2: return launch_tile<256, 256, 64, 2, 2, 4, EPI>(p, stream);
+    case 3: return launch_tile<256, 256, 32, 4, 2, 4, EPI>(p, stream);
+    case 4: return launch_tile<128, 512, 32, 3, 2, 4, EPI>(p, stream);
     case 21: return launch_tile<64, 64, 64, 4, 2, 1, EPI>(p, stream);
     case 22: return launch_tile<32, 128, 64, 4, 1, 2, EPI>(p, stream);
     // narrow-N shapes (router logits, fp32 epilogue)

@@ -546,17 +546,18 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
     // weight gradients: both operands row-major activations reduced over the group's rows
     if (!p.x_mn || !p.w_mn || p.M < 8 || p.M % 8) return hipErrorInvalidValue;
     // 256 x 256 tiles, two 64-wide slices in flight: measured against 128 x 128 tiles with two
-    // or three workgroups per CU and three 32-wide slices in flight (3-10% slower at DeepSeek-V3
-    // and Mixtral shapes)
-#ifndef MOE_BWD_KSEG_CFG
-#define MOE_BWD_KSEG_CFG 0
-#endif
+    // or three workgroups per CU and three 32-wide slices in flight (routed dW13 at DeepSeek-V3
+    // 1079-1132 us against 985)
+#ifdef MOE_BWD_KSEG_CFG
+    // tuning alternatives (not chosen by the launcher)
     switch (MOE_BWD_KSEG_CFG) {
       case 1: return launch_bwd<128, 128, 64, 2, 2, 2, true, true, BWD_KSEG, 2>(p, stream);
       case 3: return launch_bwd<128, 128, 32, 4, 2, 2, true, true, BWD_KSEG, 2>(p, stream);
       case 4: return launch_bwd<128, 128, 32, 3, 2, 2, true, true, BWD_KSEG, 3>(p, stream);
-      default: return launch_bwd<256, 256, 64, 2, 4, 2, true, true, BWD_KSEG, 1>(p, stream);
+      default: break;
     }
+#endif
+    return launch_bwd<256, 256, 64, 2, 4, 2, true, true, BWD_KSEG, 1>(p, stream);
   }
   return hipErrorInvalidValue;
 }
