@@ -569,6 +569,19 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     permute_ms = e0.elapsed_time(e1) / reps
+
+    # the routed experts alone (moe_grouped_ffn on the permuted rows, no shared expert): the
+    # routed-only grouped-GEMM figure; the shape describes exactly the batch's local rows
+    log("timing the routed grouped MLP alone")
+    n_routed = int(p_offsets[-1].item())
+    routed_ms = None
+    if n_routed > 0:
+        r_sh = sh.replace(T=n_routed, top_k=1, F_shared=0, fusion=0)
+        r_y = torch.empty((n_routed, sh.d), dtype=torch.bfloat16, device="cuda:0")
+        r_ws = moe.alloc_workspace(r_sh, moe.MOE_WS_FFN, "cuda:0")
+        routed_ms = timed_median(lambda: moe.moe_grouped_ffn(r_sh, p_x_perm, p_offsets, layer.w13, layer.w2, r_y,
+                                                             r_ws), 20)
+        del r_y, r_ws
     del p_x_perm
 
     # algorithmic work of this batch (from the routing the GPU produced)
@@ -614,6 +627,8 @@ def main():
                    "local_rows": n_loc, "parallelism": "one expert-parallel rank's share on 1 GPU"},
         "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
         "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "routed_gemm_ms": routed_ms,
+        "routed_gemm_tflops": (6.0 * d * F * n_loc / (routed_ms * 1e-3) / 1e12) if routed_ms else None,
         "permute_gbs": perm_bytes / (permute_ms * 1e-3) / 1e9,
         "permute_ms": permute_ms,
         "permute_in_layer": "row copy folded into the up-projection (token rows read through row_token)",

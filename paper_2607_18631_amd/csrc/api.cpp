@@ -41,6 +41,16 @@ int64_t capacity(const moe_shape_t* s) {
   return s->T * (int64_t)(s->top_k < s->E_local ? s->top_k : s->E_local);
 }
 
+// Expected rows per local expert of a layer call (tile-shape choice only; the real counts stay
+// on the device): T * top_k / E under uniform routing, at most the expert capacity in the masked
+// layout.  The standalone grouped-FFN entry points take their capacity / E_local instead (their
+// rows fill the capacity they are given, e.g. the shared expert as one group of T rows).
+int64_t expected_rows(const moe_shape_t* s) {
+  int64_t r = std::max<int64_t>(1, s->T * s->top_k / std::max(1, s->E));
+  if (s->expert_capacity > 0) r = std::min<int64_t>(r, s->expert_capacity);
+  return r;
+}
+
 int check_shape(const moe_shape_t* s) {
   if (!s) return fail(MOE_ERR_INVALID_ARG, "shape is NULL");
   if (s->T < 0) return fail(MOE_ERR_INVALID_ARG, "T (%lld) < 0", (long long)s->T);
@@ -773,9 +783,7 @@ int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_ro
   r.offsets = C > 0 ? counts : offsets;
   r.groups = s->E_local;
   r.rows = cap;
-  int64_t hint = std::max<int64_t>(1, T * s->top_k / E);
-  if (C > 0) hint = std::min<int64_t>(hint, C);
-  r.rows_hint = hint;
+  r.rows_hint = expected_rows(s);
   r.seg_stride = C;
   r.d = d;
   r.F = F;
@@ -951,10 +959,8 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     gather.row_index = row_token;
     gather.x_rows = shape->T;
   }
-  // expected rows per local expert (uniform routing): T * top_k / E, at most the capacity
-  int64_t rows_hint = std::max<int64_t>(1, shape->T * shape->top_k / shape->E);
+  const int64_t rows_hint = expected_rows(shape);
   const int C = shape->expert_capacity;
-  if (C > 0) rows_hint = std::min<int64_t>(rows_hint, C);
   // the masked-decode layout hands the GEMM the per-expert counts and the segment stride
   CHECK(do_ffn(fused_gather ? x : x_perm, C > 0 ? counts : offsets, shape->E_local, capacity(shape), w13, w2,
                shape->d, shape->F, at<void>(ws, L.act), y_perm, st, mark, MOE_STEP_FFN_DOWN,
