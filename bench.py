@@ -408,6 +408,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-routed-gemm", action="store_true",
+                    help="skip the routed-only grouped-MLP timing (it launches the layer's GEMM kernels "
+                         "again, so kernel profiles of the layer pass this)")
     ap.add_argument("--cpu-sample", type=int, default=8192, help="tokens of the oracle CPU baseline sample")
     ap.add_argument("--crossover", action="store_true",
                     help="the paper's RQ4 kernel-crossover sweep (E=64, d=2048, F=1408, top-2, 8 local experts, "
@@ -572,10 +575,10 @@ def main():
 
     # the routed experts alone (moe_grouped_ffn on the permuted rows, no shared expert): the
     # routed-only grouped-GEMM figure; the shape describes exactly the batch's local rows
-    log("timing the routed grouped MLP alone")
     n_routed = int(p_offsets[-1].item())
     routed_ms = None
-    if n_routed > 0:
+    if n_routed > 0 and not args.no_routed_gemm:
+        log("timing the routed grouped MLP alone")
         r_sh = sh.replace(T=n_routed, top_k=1, F_shared=0, fusion=0)
         r_y = torch.empty((n_routed, sh.d), dtype=torch.bfloat16, device="cuda:0")
         r_ws = moe.alloc_workspace(r_sh, moe.MOE_WS_FFN, "cuda:0")
