@@ -432,8 +432,8 @@ def main():
                     help="run one plain device copy of this many MiB first (reference dispatch for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs the MoE-layer forward of one expert-parallel rank on ONE GPU; "
-                                   "--gpus must be 1 (multi-GPU sharding is described, not built)"}))
+        print(json.dumps({"error": "this library runs one expert-parallel rank's share of the MoE layer on ONE "
+                                   "GPU; --gpus must be 1 (the multi-GPU sharding is a design, not implemented)"}))
         sys.exit(2)
 
     import numpy as np
