@@ -384,11 +384,20 @@ def cpu_baseline(inputs, sample_tokens):
     import oracle
     sh = inputs["shape"]
     n = min(sample_tokens, sh.T)
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        info = threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] or [1])
+        blas = ", ".join(f"{i.get('internal_api')} {i.get('version')}" for i in info) or blas
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu_model)
+    except OSError:  # pragma: no cover
+        pass
     t0 = time.perf_counter()
     xd = oracle.bf16_to_f64(inputs["x"][:n])
     idx, w, _ = oracle.route(xd, oracle.bf16_to_f64(inputs["w_router"]), sh, inputs.get("bias"))
@@ -397,6 +406,7 @@ def cpu_baseline(inputs, sample_tokens):
     dt = time.perf_counter() - t0
     assert np.isfinite(out).all()
     return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model, "blas": blas, "host_cpus": len(os.sched_getaffinity(0)),
             "sample": f"first {n} of {sh.T} tokens of the same batch: fp64 routing, expert and shared SwiGLU "
                       f"MLPs and combine ({dt:.1f} s)"}
 
