@@ -597,6 +597,13 @@ def main():
         del r_y, r_ws
     del p_x_perm
 
+    # practical HBM ceiling: a plain 1 GiB device-to-device copy (bytes read + written per second)
+    log("timing a 1 GiB device copy")
+    c_src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda:0")
+    c_dst = torch.empty_like(c_src)
+    copy_ms = timed_median(lambda: c_dst.copy_(c_src), 10, warmup=3)
+    del c_src, c_dst
+
     # algorithmic work of this batch (from the routing the GPU produced)
     offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
     slot_row = layer.region(moe.MOE_REGION_SLOT_ROW, torch.int32, (sh.T, sh.top_k)).cpu().numpy()
@@ -646,6 +653,7 @@ def main():
         "permute_ms": permute_ms,
         "permute_in_layer": "row copy folded into the up-projection (token rows read through row_token)",
         "combine_gbs": comb_bytes / (avg[s["combine"]] * 1e-3) / 1e9,
+        "copy_gbs": 2.0 * (1 << 30) / (copy_ms * 1e-3) / 1e9,
         "layer_hbm_gbs": layer_bytes / (ms_step * 1e-3) / 1e9,
         "active_local_experts": active,
         "step_ms": {n: round(float(med[i]), 5) for n, i in s.items()},
