@@ -1,4 +1,4 @@
-// Device-side helpers shared by the gfx950 kernels of the MoE-layer forward.
+// Device-side helpers shared by the gfx950 kernels of the MoE layer (forward and backward).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -15,17 +15,20 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
 
-// float32 -> bf16, round to nearest, ties to even (NaN stays NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two float32 -> bf16 (round to nearest, ties to even; NaN stays NaN), packed lo | hi << 16:
+// one gfx950 v_cvt_pk_bf16_f32.  An integer-arithmetic rounding costs ~8 VALU instructions per
+// value, which made the bf16 epilogues of short-K tiles VALU-bound (a 256 x 256 weight-gradient
+// tile spent ~2.7 us per 32-row block converting).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
-}
+// float32 -> bf16 bits of one value (same rounding)
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) { return pack_bf16x2(f, 0.0f) & 0xffffu; }
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
