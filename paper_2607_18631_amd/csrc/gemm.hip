@@ -388,6 +388,8 @@ __device__ __forceinline__ int frag_wrow(int wn, int b) {
   return wn * (BN / WGN) + b * 32;
 }
 
+// silu(g) = g / (1 + e^-g) is taken as g * rcp(1 + e^-g) (v_rcp_f32, 1 ulp) in every epilogue: the
+// result is rounded to bf16 next, and an IEEE division costs ~10 VALU instructions per element.
 // Store one wave's FM x FN accumulator fragments of tile t.  Lane holds token row
 // trow + astride a + (lane & 31) and output features fcol + 32 b + 8 q + 4 (lane >> 5) + 0..3.
 // SwiGLU pairs fragment b (gate) with b + FN/2 (up): Y = bf16(silu(gate) * up).
@@ -416,7 +418,7 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float h = acc[a][b][4 * q + e], u = acc[a][b + FN / 2][4 * q + e];
-            const float sg = 1.0f / (1.0f + __expf(-h));
+            const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-h));
             const float silu = h * sg;
             av[e] = silu * u;
             du[e] = da[e] * silu;
@@ -446,7 +448,7 @@ __device__ __forceinline__ void store_tile(const GemmProblem& p, const f32x16 (&
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             float gt = acc[a][b][4 * q + e], up = acc[a][b + FN / 2][4 * q + e];
-            o[e] = gt / (1.0f + __expf(-gt)) * up;
+            o[e] = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
           }
           uint2 v;
           v.x = pack_bf16x2(o[0], o[1]);
@@ -518,7 +520,7 @@ __device__ __forceinline__ void store_tile_staged(const GemmProblem& p, const f3
         for (int e = 0; e < 4; ++e) {
           if (EPI == EPI_SWIGLU) {
             const float gt = acc[a][b][4 * q + e], up = acc[a][b + FN / 2][4 * q + e];
-            o[e] = gt / (1.0f + __expf(-gt)) * up;
+            o[e] = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
           } else {
             o[e] = acc[a][b][4 * q + e];
           }
