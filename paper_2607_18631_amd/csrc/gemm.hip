@@ -126,6 +126,7 @@ constexpr int BAND_M = MOE_BAND_M;   // m-tiles per band of the tile order
 // the slowest index, so the workgroups of one XCD work on one K chunk of the weights.
 struct TileSpace {
   int groups, tiles_n, tiles_x, total;
+  int bmx;                   // m-tile height of the extra group
   int base_total;            // (m, n) tiles
   int nk, kchunk;            // K slices; slices per chunk
   int seg_stride;            // > 0: group g owns rows [g * seg_stride, g * seg_stride + s_off[g])
@@ -178,7 +179,8 @@ __device__ TileSpace build_tile_space(const GemmProblem& p, int outn, int* s_off
   if (tid == 0) s_tp[groups] = total_r;
   __syncthreads();
   // the extra group's tiles sit among the grouped ones (see extra_position)
-  ts.tiles_x = p.rows2 > 0 ? ((p.rows2 + BM - 1) / BM) * ts.tiles_n : 0;
+  ts.bmx = (p.rows2_tile > 0 && p.rows2_tile < BM) ? p.rows2_tile : BM;
+  ts.tiles_x = p.rows2 > 0 ? ((p.rows2 + ts.bmx - 1) / ts.bmx) * ts.tiles_n : 0;
   ts.base_total = total_r + ts.tiles_x;
   ts.nk = (p.K + BK - 1) / BK;
   const int ksplit = p.ksplit > 1 ? p.ksplit : 1;
@@ -274,7 +276,8 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
     d.stok = p.scatter_token;
     d.sw = p.scatter_weight;
   }
-  const int mt = (d.row_end - row0g + BM - 1) / BM;
+  const int bmg = extra ? ts.bmx : BM;                  // m-tile height of this group
+  const int mt = (d.row_end - row0g + bmg - 1) / bmg;
   // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
   // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
   // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
@@ -284,7 +287,8 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
   const int in_band = local - band * BAND_M * ts.tiles_n;
   const int mi = bm0 + in_band % bmt;
   d.ni = in_band / bmt;
-  d.row0 = row0g + mi * BM;
+  d.row0 = row0g + mi * bmg;
+  if (bmg < BM) d.row_end = min(d.row0 + bmg, d.row_end);   // the extra group's shorter tiles
   return d;
 }
 
@@ -813,7 +817,8 @@ hipError_t launch_persistent(const void* fn, OccCache& occ, int nth, size_t lds,
   const int64_t tiles_n = (p.N + outn - 1) / outn;
   const int64_t groups = p.offsets ? p.groups : 1;
   const int64_t rows = p.offsets ? p.max_rows : p.rows_single;
-  const int64_t upper = tiles_n * ((rows + bm - 1) / bm + groups + (p.rows2 + bm - 1) / bm) *
+  const int bmx = (p.rows2_tile > 0 && p.rows2_tile < bm) ? p.rows2_tile : bm;
+  const int64_t upper = tiles_n * ((rows + bm - 1) / bm + groups + (p.rows2 + bmx - 1) / bmx) *
                         (p.ksplit > 1 ? p.ksplit : 1);
   const int64_t resident = (int64_t)cu_count() * per_cu;
   int64_t grid = upper < resident ? upper : resident;
@@ -946,12 +951,13 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   // skewed workload stay on 256 x 256.  The backward's recomputed up-projection of the routed
   // experts alone (tier 128 x 256) takes 320-row tiles at DeepSeek-V3 (627 -> 521 us).
   int cfg_swiglu_bwd = tier;
+  int rows2_tile = 0;
   if ((tier == 5 || tier == 6) && p.rows_hint > 0) {
     const double cus = cu_count();
     const int64_t groups = p.offsets ? p.groups : 1;
     const double mu = (double)p.rows_hint;
     const double sigma = groups > 1 ? std::sqrt(mu) : 0.0;
-    auto mtiles = [&](int bm) {                          // expected m-tiles of the launch
+    auto grouped_mtiles = [&](int bm) {                  // expected m-tiles of the groups
       double per_group = 0;
       if (sigma == 0) {
         per_group = std::ceil(mu / bm);
@@ -960,8 +966,9 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
         for (int j = 0; j <= jmax; ++j)                   // E[ceil(m / bm)] = sum_j P(m > j bm)
           per_group += 0.5 * std::erfc((j * bm - mu) / (sigma * std::sqrt(2.0)));
       }
-      return per_group * groups + std::ceil((double)p.rows2 / bm);
+      return per_group * groups;
     };
+    auto mtiles = [&](int bm) { return grouped_mtiles(bm) + std::ceil((double)p.rows2 / bm); };
     // rounds of the persistent grid; an expected count a few hundredths of a round above a
     // whole number (the normal tail of the row counts) is that whole number
     auto rounds = [&](double tiles) { return std::max(1.0, std::ceil(tiles / cus - 0.05)); };
@@ -980,13 +987,26 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
       if (c8 < c6 && c8 <= c7) cfg_bf16 = 8;
       else if (c7 < c6) cfg_bf16 = 7;
     }
+    // On 320-row tiles, a dense extra group (the shared expert) is tiled 256 rows high when that
+    // adds no round: its tiles then carry the 8 live token blocks the routed ones do (the routed
+    // experts' ~256 rows), instead of 10.  DeepSeek-V3 shapes: up-projection 928 -> 1024 tiles
+    // (4 rounds either way), down-projection 1624 -> 1792 (7 rounds either way).
+    const int my_cfg = p.epi == EPI_SWIGLU ? cfg_swiglu : p.epi == EPI_BF16 ? cfg_bf16 : 0;
+    if (my_cfg == 8 && p.rows2 > 256) {
+      const double cols = p.epi == EPI_SWIGLU ? tn : tn256;
+      const double g320 = grouped_mtiles(320);
+      if (rounds((g320 + std::ceil(p.rows2 / 256.0)) * cols) <= rounds((g320 + std::ceil(p.rows2 / 320.0)) * cols))
+        rows2_tile = 256;
+    }
   }
 #ifdef MOE_GEMM_SWEEP
   if (g_force_cfg[EPI_SWIGLU] >= 0) cfg_swiglu = g_force_cfg[EPI_SWIGLU];
   if (g_force_cfg[EPI_BF16] >= 0) cfg_bf16 = g_force_cfg[EPI_BF16];
 #endif
+  GemmProblem q = p;
+  q.rows2_tile = rows2_tile;
   switch (p.epi) {
-    case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, p, stream);
+    case EPI_SWIGLU: return launch_cfg<EPI_SWIGLU>(cfg_swiglu, q, stream);
     case EPI_SWIGLU_BWD:
       if (!p.dact || !p.act_out || p.rows2 > 0 || p.ldy != 2 * (int64_t)p.N) return hipErrorInvalidValue;
       switch (cfg_swiglu_bwd) {      // the tiers of the forward up-projection (same operand shapes)
@@ -995,7 +1015,7 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
         case 8: return launch_tile<320, 256, 64, 2, 2, 4, EPI_SWIGLU_BWD>(p, stream);
         default: return launch_tile<256, 256, 64, 2, 4, 2, EPI_SWIGLU_BWD>(p, stream);
       }
-    case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, p, stream);
+    case EPI_BF16: return launch_cfg<EPI_BF16>(cfg_bf16, q, stream);
     case EPI_SCATTER:
       if (p.scatter_rows < 1) return hipErrorInvalidValue;
       switch (tier) {      // the tiers of the bf16 epilogue (same operand shapes)

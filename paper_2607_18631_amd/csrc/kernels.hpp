@@ -45,6 +45,8 @@ struct GemmProblem {
   const bf16_t* W2;
   void* Y2;
   int32_t rows2;
+  int32_t rows2_tile;         // m-tile height of the extra group: 0 = the launch's, else a multiple
+                              // of 32 below it (its tiles then run with dead blocks)
   // K split (EPI_F32, one group, no extra group): ksplit > 1 runs the K range in ksplit
   // chunks, chunk c writing its fp32 partial product at Y + c * y_split_stride
   int32_t ksplit;
