@@ -557,6 +557,10 @@ hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream) {
     // 256 x 256 tiles, two 64-wide slices in flight: measured against 128 x 128 tiles with two
     // or three workgroups per CU and three 32-wide slices in flight (routed dW13 at DeepSeek-V3
     // 1079-1132 us against 985)
+    // the router's weight gradient (float32 K-split partials, M = the expert count): 128 x 128
+    // tiles, two workgroups per CU, 4x the tiles of 256 x 256 ones for its few output tiles
+    // (DeepSeek-V3: 256 x 7168 outputs over 9 token chunks, 76 -> 59 us)
+    if (p.Yf) return launch_bwd<128, 128, 64, 2, 2, 2, true, true, BWD_KSEG, 2>(p, stream);
 #ifdef MOE_BWD_KSEG_CFG
     // tuning alternatives (not chosen by the launcher)
     switch (MOE_BWD_KSEG_CFG) {
