@@ -270,13 +270,52 @@ __global__ __launch_bounds__(64 * kWaves) void k_unpermute_sum(UnpermuteSumProbl
           acc[u][2 * e + 1] += bf_hi(y[u][e]);
         }
     };
+    // two rows' loads in flight at a time; the additions keep the slot order (then extra0, extra1)
+    auto add_two = [&](const bf16_t* r0, const bf16_t* r1) {
+      u32x4 y0[U], y1[U];
 #pragma unroll
-    for (int a = 0; a < 16; ++a) {
-      if (a >= nact) break;
-      add_row(p.rows + (int64_t)rows[a] * p.d);
+      for (int u = 0; u < U; ++u) {
+        const int v = v0 + u * 64 + lane;
+        y0[u] = v < nvec ? ld16(r0 + v * 8) : u32x4{0, 0, 0, 0};
+        y1[u] = v < nvec ? ld16(r1 + v * 8) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[u][2 * e] += bf_lo(y0[u][e]);
+          acc[u][2 * e + 1] += bf_hi(y0[u][e]);
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[u][2 * e] += bf_lo(y1[u][e]);
+          acc[u][2 * e + 1] += bf_hi(y1[u][e]);
+        }
+    };
+    int a = 0;
+#pragma unroll
+    for (int pr = 0; pr < 8; ++pr) {
+      if (a + 1 >= nact) break;
+      add_two(p.rows + (int64_t)rows[a] * p.d, p.rows + (int64_t)rows[a + 1] * p.d);
+      a += 2;
     }
-    if (p.extra0) add_row(p.extra0 + t * p.d);
-    if (p.extra1) add_row(p.extra1 + t * p.d);
+    if (a < nact) {
+      // an odd last row pairs with the first extra row when there is one
+      if (p.extra0) {
+        add_two(p.rows + (int64_t)rows[a] * p.d, p.extra0 + t * p.d);
+        if (p.extra1) add_row(p.extra1 + t * p.d);
+      } else {
+        add_row(p.rows + (int64_t)rows[a] * p.d);
+        if (p.extra1) add_row(p.extra1 + t * p.d);
+      }
+    } else if (p.extra0 && p.extra1) {
+      add_two(p.extra0 + t * p.d, p.extra1 + t * p.d);
+    } else {
+      if (p.extra0) add_row(p.extra0 + t * p.d);
+      if (p.extra1) add_row(p.extra1 + t * p.d);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = v0 + u * 64 + lane;
