@@ -42,6 +42,9 @@ CASES = {
     # 256 rows per expert on average over 32 experts, d and 2F multiples of 64: the routed dX runs
     # on the 320-row tile without K-tail code, the recomputed up-projection on 320-row tiles
     "tile320_rows": (S(T=1024, d=2048, E=32, top_k=8, F=1024, E_local=32), None, 0.0),
+    # the logit partials of a K split with uneven chunks (16 chunks of 7 slices of 64, the last 5,
+    # its last slice 24 wide) summed again for the gate gradients; router dW over token chunks
+    "router_ksplit_ragged": (S(T=4096, d=7000, E=128, top_k=8, F=64, E_local=8, e_begin=40), None, 0.0),
 }
 GRADS = ("dx", "dw_router", "dw13", "dw2", "dws13", "dws2")
 

@@ -39,6 +39,9 @@ SMALL = {
     # 256 rows per expert on average over 32 experts with K tails in both projections (d, F not
     # multiples of 64): enough tiles that both projections take 320-row tiles, with tail slices
     "tile320_ktail": (S(T=1024, d=2000, E=32, top_k=8, F=1000, E_local=32), None, 0.0),
+    # router logits on 256 x 256 tiles with a K split whose chunks are uneven: 110 slices of 64
+    # (the last 24 wide) in 16 chunks of 7, the last chunk 5 slices
+    "router_ksplit_ragged": (S(T=4096, d=7000, E=128, top_k=8, F=64, E_local=8, e_begin=40), None, 0.0),
     # the kernel-crossover shape at expert multiplicities 4 and 32
     "crossover_me4": (wl.crossover(4).shape, None, 0.0),
     "crossover_me32": (wl.crossover(32).shape, None, 0.0),
