@@ -167,6 +167,41 @@ def _threads() -> int:
     return max(1, min(16, n))
 
 
+def expert_tensors(wl: Workload | str, le: int, seed: int | None = None, out13=None, out2=None):
+    """bf16 bits of local expert ``le``'s weights: ``w13 [2F, d]`` (rows [0,F) = W1 gate, rows
+    [F,2F) = W3 up) and ``w2 [d, F]``, drawn from the streams of global expert e_begin + le."""
+    if isinstance(wl, str):
+        wl = WORKLOADS[wl]
+    sh = wl.shape
+    seed = wl.seed if seed is None else seed
+    d, F = sh.d, sh.F
+    ge = sh.e_begin + le
+    w13 = np.empty((2 * F, d), np.uint16) if out13 is None else out13
+    w2 = np.empty((d, F), np.uint16) if out2 is None else out2
+    _normal_bf16(seed, _TID_W1, ge, (F, d), d ** -0.5, w13[:F])
+    _normal_bf16(seed, _TID_W3, ge, (F, d), d ** -0.5, w13[F:])
+    _normal_bf16(seed, _TID_W2, ge, (d, F), F ** -0.5, w2)
+    return w13, w2
+
+
+def shared_tensors(wl: Workload | str, seed: int | None = None):
+    """bf16 bits of the shared expert's weights ``ws13 [2F_s, d]`` and ``ws2 [d, F_s]`` (None, None
+    without a shared expert)."""
+    if isinstance(wl, str):
+        wl = WORKLOADS[wl]
+    sh = wl.shape
+    seed = wl.seed if seed is None else seed
+    d, Fs = sh.d, sh.F_shared
+    if Fs <= 0:
+        return None, None
+    ws13 = np.empty((2 * Fs, d), np.uint16)
+    ws2 = np.empty((d, Fs), np.uint16)
+    _normal_bf16(seed, _TID_WS1, 0, (Fs, d), d ** -0.5, ws13[:Fs])
+    _normal_bf16(seed, _TID_WS3, 0, (Fs, d), d ** -0.5, ws13[Fs:])
+    _normal_bf16(seed, _TID_WS2, 0, (d, Fs), Fs ** -0.5, ws2)
+    return ws13, ws2
+
+
 def make_inputs(wl: Workload | str, T: int | None = None, seed: int | None = None,
                 with_experts: bool = True) -> dict:
     """Draw every input of workload ``wl`` (optionally with a different token count).
@@ -180,7 +215,7 @@ def make_inputs(wl: Workload | str, T: int | None = None, seed: int | None = Non
         wl = WORKLOADS[wl]
     sh = wl.shape if T is None else wl.shape.replace(T=T)
     seed = wl.seed if seed is None else seed
-    d, F, Fs = sh.d, sh.F, sh.F_shared
+    d, F = sh.d, sh.F
     out = {"shape": sh, "workload": wl.name, "seed": seed}
     jobs = []
     out["x"] = np.empty((sh.T, d), np.uint16)
@@ -192,23 +227,15 @@ def make_inputs(wl: Workload | str, T: int | None = None, seed: int | None = Non
         w13 = np.empty((sh.E_local, 2 * F, d), np.uint16)
         w2 = np.empty((sh.E_local, d, F), np.uint16)
         for le in range(sh.E_local):
-            ge = sh.e_begin + le
-            jobs.append(lambda le=le, ge=ge: _normal_bf16(seed, _TID_W1, ge, (F, d), d ** -0.5, w13[le, :F]))
-            jobs.append(lambda le=le, ge=ge: _normal_bf16(seed, _TID_W3, ge, (F, d), d ** -0.5, w13[le, F:]))
-            jobs.append(lambda le=le, ge=ge: _normal_bf16(seed, _TID_W2, ge, (d, F), F ** -0.5, w2[le]))
+            jobs.append(lambda le=le: expert_tensors(wl, le, seed, w13[le], w2[le]))
         out["w13"], out["w2"] = w13, w2
-        if Fs > 0:
-            ws13 = np.empty((2 * Fs, d), np.uint16)
-            ws2 = np.empty((d, Fs), np.uint16)
-            jobs.append(lambda: _normal_bf16(seed, _TID_WS1, 0, (Fs, d), d ** -0.5, ws13[:Fs]))
-            jobs.append(lambda: _normal_bf16(seed, _TID_WS3, 0, (Fs, d), d ** -0.5, ws13[Fs:]))
-            jobs.append(lambda: _normal_bf16(seed, _TID_WS2, 0, (d, Fs), Fs ** -0.5, ws2))
-            out["ws13"], out["ws2"] = ws13, ws2
-        else:
-            out["ws13"] = out["ws2"] = None
+        shared = {}
+        jobs.append(lambda: shared.update(zip(("ws13", "ws2"), shared_tensors(wl, seed))))
     with ThreadPoolExecutor(_threads()) as ex:
         for f in [ex.submit(j) for j in jobs]:
             f.result()
+    if with_experts:
+        out["ws13"], out["ws2"] = shared["ws13"], shared["ws2"]
     return out
 
 

@@ -79,17 +79,18 @@ def test_fusion_matrix_small(name):
 @pytest.mark.parametrize("name", ["dsv3", "mixtral", "k2decode"])
 def test_fused_combine_full_workload(name):
     """Both folds at the full workload sizes (the benchmark's fusion-matrix configuration):
-    sampled output rows against the oracle."""
+    every output token against the oracle."""
     print(f"[fusion] full workload {name}: generating inputs", flush=True)
     inputs = wl.make_inputs(name)
     sh = inputs["shape"]
     layer, out = _layer_out(inputs, wl.FUSION_VARIANTS["both"])
-    rng = np.random.default_rng(7)
-    toks = np.sort(rng.choice(sh.T, size=min(sh.T, 32), replace=False))
-    ref, _ = _oracle_out(inputs, layer, toks)
-    err = rel_fro(oracle.bf16_to_f64(out[toks]), ref)
-    print(f"[fusion] {name} both: rel_fro={err:.3e} on {toks.size} tokens", flush=True)
-    assert err <= REL_TOL
+    ref, _ = _oracle_out(inputs, layer)
+    got = oracle.bf16_to_f64(out)
+    err = rel_fro(got, ref)
+    blk = max(rel_fro(got[i:i + 128], ref[i:i + 128]) for i in range(0, sh.T, 128))
+    print(f"[fusion] {name} both: rel_fro={err:.3e} over all {sh.T} tokens (worst 128-token block {blk:.3e})",
+          flush=True)
+    assert err <= REL_TOL and blk <= 2 * REL_TOL
     # the folded combine is the unfolded one up to summation order and one bf16 rounding
     _, base = _layer_out(inputs, 0)
-    assert rel_fro(oracle.bf16_to_f64(out), oracle.bf16_to_f64(base)) <= REL_TOL
+    assert rel_fro(got, oracle.bf16_to_f64(base)) <= REL_TOL

@@ -13,6 +13,7 @@ import oracle
 from paper_2607_18631_amd import moe
 from paper_2607_18631_amd import workloads as wl
 
+import parity_util
 from parity_util import (REL_TOL, check_routing, dev_bits, oracle_routing_with_gpu_ties, rel_fro,
                          run_route)
 
@@ -46,7 +47,6 @@ def _regions(layer):
         "offsets": g(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)),
         "row_token": g(moe.MOE_REGION_ROW_TOKEN, torch.int32, (cap,)),
         "slot_row": g(moe.MOE_REGION_SLOT_ROW, torch.int32, (T, k)),
-        "y_perm": dev_bits(layer.region(moe.MOE_REGION_Y_PERM, torch.bfloat16, (cap, sh.d))),
     }
 
 
@@ -79,17 +79,11 @@ def test_masked_layer_parity(name):
     np.testing.assert_array_equal(reg["topk_idx"], g_idx)
     counts, row_token = _check_masked_permutation(sh, reg, g_idx)
     dropped = int(np.maximum(counts - C, 0).sum())
-    # per-expert rows of the valid prefix of each segment
+    # per-expert rows of the valid prefix of each segment (only those rows are decoded: the rest
+    # of a segment is never written)
     xd = oracle.bf16_to_f64(inputs["x"])
-    y = oracle.bf16_to_f64(reg["y_perm"])
-    for e in range(sh.E_local):
-        n = min(int(counts[e]), C)
-        if n == 0:
-            continue
-        rows = slice(e * C, e * C + n)
-        ref = oracle.swiglu_ffn(xd[row_token[rows]], oracle.bf16_to_f64(inputs["w13"][e]),
-                                oracle.bf16_to_f64(inputs["w2"][e]))
-        assert rel_fro(y[rows], ref) <= REL_TOL, (e, rel_fro(y[rows], ref))
+    segs = parity_util.expert_segments(sh, counts, reg["offsets"])
+    parity_util.check_expert_rows(inputs, xd, segs, parity_util.live_y_rows(layer, segs), row_token)
     # layer output: the kept slots of the whole batch's routing
     idx, w = oracle_routing_with_gpu_ties(o_idx, o_w, keys64, g_idx, near, sh)
     keep = oracle.keep_mask(idx, sh.e_begin, sh.E_local, C)
