@@ -21,7 +21,8 @@
  *    bf16 tensors are row-major, contiguous, 16-byte aligned; int32 / float
  *    arrays are contiguous and 4-byte aligned.  The library allocates no device
  *    memory on any call path; scratch space comes from the caller's workspace,
- *    whose size moe_workspace_size() returns.
+ *    whose size moe_workspace_size() returns (moe_permute_noalloc takes none: its
+ *    scratch is a fixed device array of the library).
  *  - Streams.  `stream` is a hipStream_t passed as an opaque pointer (NULL = the
  *    legacy default stream).  Each call validates its arguments on the host; on
  *    success it enqueues its kernels on `stream` and returns without waiting.
@@ -195,6 +196,19 @@ int moe_route(const moe_shape_t* shape, const void* x, const void* w_router, con
 int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x,
                 int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* slot_row,
                 void* x_perm, void* ws, size_t ws_bytes, void* stream);
+
+/* moe_permute without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops that forbid allocation).  Same arguments,
+ * results and layouts as moe_permute; its scratch (per-chunk counts and bases,
+ * moe_workspace_size(shape, MOE_WS_PERMUTE) bytes) lives in a fixed 1 MiB device array owned
+ * by the library, one per device, kept until the process ends.  Larger requests (T / 64 *
+ * E_local > 131072, e.g. E_local = 128 with T > 65536) return MOE_ERR_UNSUPPORTED.  The call
+ * allocates nothing; the first call on a device looks up the array's address there.
+ * Every call on one GPU shares that GPU's array: calls that may overlap on one GPU (other
+ * streams, other threads) race on it and must be ordered by the caller. */
+int moe_permute_noalloc(const moe_shape_t* shape, const int32_t* topk_idx, const void* x,
+                        int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* slot_row,
+                        void* x_perm, void* stream);
 
 /* Grouped SwiGLU expert MLP (step 9): for every local expert e and every row r in
  * [offsets[e], offsets[e+1]):  y_perm[r] = W2_e (silu(W1_e x_perm[r]) * (W3_e x_perm[r])).

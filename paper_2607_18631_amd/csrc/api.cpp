@@ -619,6 +619,28 @@ int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x
   return ok();
 }
 
+int moe_permute_noalloc(const moe_shape_t* shape, const int32_t* topk_idx, const void* x, int32_t* counts,
+                        int32_t* offsets, int32_t* row_token, int32_t* slot_row, void* x_perm, void* stream) {
+  CHECK(check_shape(shape));
+  const size_t need = ws_permute(shape);
+  if (need > moe::kPermuteScratchBytes)
+    return fail(MOE_ERR_UNSUPPORTED,
+                "moe_permute_noalloc needs %zu bytes of scratch for T=%lld, E_local=%d; its fixed scratch holds %zu",
+                need, (long long)shape->T, shape->E_local, moe::kPermuteScratchBytes);
+  if (shape->T == 0) return ok();
+  CHECK(check_ptr(topk_idx, 4, "topk_idx"));
+  CHECK(check_ptr(x, 16, "x"));
+  CHECK(check_ptr(counts, 4, "counts"));
+  CHECK(check_ptr(offsets, 4, "offsets"));
+  CHECK(check_ptr(row_token, 4, "row_token"));
+  CHECK(check_ptr(slot_row, 4, "slot_row"));
+  CHECK(check_ptr(x_perm, 16, "x_perm"));
+  void* scratch = nullptr;
+  CHECK(hip_status(moe::permute_scratch(&scratch), "scratch address lookup (hipGetSymbolAddress)"));
+  CHECK(do_permute(shape, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, scratch, as_stream(stream)));
+  return ok();
+}
+
 int moe_grouped_ffn(const moe_shape_t* shape, const void* x_perm, const int32_t* offsets, const void* w13,
                     const void* w2, void* y_perm, void* ws, size_t ws_bytes, void* stream) {
   CHECK(check_shape(shape));

@@ -172,6 +172,12 @@ struct CombineProblem {
 };
 hipError_t launch_combine(const CombineProblem& p, hipStream_t stream);
 
+// Scratch of moe_permute_noalloc: a device array of this many bytes owned by the library (one
+// per device, shared by every call on it).  permute_scratch returns its device address on the
+// current device (looked up once per device).
+constexpr size_t kPermuteScratchBytes = size_t(1) << 20;
+hipError_t permute_scratch(void** ptr);
+
 // The row copy of the permutation alone: x_perm[slot_row[t, j]] = x[t] for every local slot.
 hipError_t launch_gather(const PermuteProblem& p, hipStream_t stream);
 

@@ -21,6 +21,8 @@
 // slot column j' and every bit b of the local expert id, one ballot gives the lanes whose
 // slot j' has bit b set; AND-ing the matching ballots (or their complements) yields the
 // lanes whose slot j' holds exactly my expert, and the popcount below my lane is the rank.
+#include <mutex>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -246,6 +248,38 @@ hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*bet
   if (p.x_perm == nullptr) return hipSuccess;
   hipLaunchKernelGGL(k_gather, dim3((unsigned)((p.T + 3) / 4)), dim3(256), 0, stream, p);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Library-owned scratch for moe_permute_noalloc: the per-chunk counts and bases live in a
+// file-scope device array instead of a caller workspace.  Each device holds its own copy;
+// host code never uses the array's name as an address (on the host it is only a symbol
+// handle), it uses the address hipGetSymbolAddress returns on that device.
+// ---------------------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[kPermuteScratchBytes];
+
+namespace {
+struct ScratchAddr {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchAddr g_scratch[kMaxDevices];
+}  // namespace
+
+hipError_t permute_scratch(void** ptr) {
+  *ptr = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  ScratchAddr& s = g_scratch[dev];
+  // once per device, with that device current (hipGetDevice above is the calling thread's)
+  std::call_once(s.once, [&] { s.err = hipGetSymbolAddress(&s.ptr, HIP_SYMBOL(scratch)); });
+  if (s.err != hipSuccess) return s.err;
+  if (s.ptr == nullptr) return hipErrorInvalidSymbol;
+  *ptr = s.ptr;
+  return hipSuccess;
 }
 
 hipError_t launch_gather(const PermuteProblem& p, hipStream_t stream) {

@@ -25,7 +25,8 @@ MOE_FUSION_SET, MOE_FUSE_GATHER, MOE_FUSE_COMBINE = 0x10, 0x1, 0x2
 
 EXPORTS = ["moe_abi_version", "moe_status_string", "moe_last_error", "moe_workspace_size",
            "moe_workspace_offset", "moe_route", "moe_permute", "moe_grouped_ffn", "moe_combine",
-           "moe_layer_forward", "moe_layer_forward_traced", "moe_grouped_ffn_backward", "moe_layer_backward"]
+           "moe_layer_forward", "moe_layer_forward_traced", "moe_grouped_ffn_backward", "moe_layer_backward",
+           "moe_permute_noalloc"]
 MOE_STEP_NAMES = ["router_gemm", "gate", "histogram", "permute", "ffn_up", "ffn_down", "shared_up",
                   "shared_down", "combine"]
 
@@ -73,6 +74,7 @@ def lib():
         L.moe_route.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_permute.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.moe_grouped_ffn.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.moe_permute_noalloc.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.moe_combine.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.moe_grouped_ffn_backward.argtypes = [sp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                                _vp]
@@ -143,6 +145,11 @@ def moe_permute(sh, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, w
     _check(lib().moe_permute(ctypes.byref(shape_c(sh)), _p(topk_idx), _p(x), _p(counts), _p(offsets),
                              _p(row_token), _p(slot_row), _p(x_perm), _p(ws), 0 if ws is None else ws.numel(),
                              _stream(stream)))
+
+
+def moe_permute_noalloc(sh, topk_idx, x, counts, offsets, row_token, slot_row, x_perm, stream=None):
+    _check(lib().moe_permute_noalloc(ctypes.byref(shape_c(sh)), _p(topk_idx), _p(x), _p(counts), _p(offsets),
+                                     _p(row_token), _p(slot_row), _p(x_perm), _stream(stream)))
 
 
 def moe_grouped_ffn(sh, x_perm, offsets, w13, w2, y_perm, ws=None, stream=None):

@@ -220,3 +220,26 @@ def test_layer_backward_pointer_and_workspace_validation():
     assert st == moe.MOE_ERR_WORKSPACE and f"required ({need_b})" in msg
     st, msg = _bwd_call(BASE.replace(gate=wl.GATE_SIGMOID), bias=FAKE)
     assert st == moe.MOE_ERR_UNSUPPORTED and "bias" in msg
+
+
+def test_permute_noalloc_validation():
+    """The allocation-free permutation validates on the host like moe_permute, and rejects a
+    request whose scratch would not fit its fixed 1 MiB device array (no HIP call is made)."""
+    L = moe.lib()
+    sp = ctypes.byref(moe.shape_c(BASE))
+    assert L.moe_permute_noalloc(sp, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+    assert "slot_row" in moe.last_error()
+    assert L.moe_permute_noalloc(sp, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
+    assert "topk_idx is NULL" in moe.last_error()
+    # 64-token chunks x E_local counts and bases: T = 2^17 tokens over 128 local experts needs 2 MiB
+    big = BASE.replace(T=2 ** 17, E=128, E_local=128, top_k=8)
+    assert moe.workspace_size(big, moe.MOE_WS_PERMUTE) > 1 << 20
+    assert L.moe_permute_noalloc(ctypes.byref(moe.shape_c(big)), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                 None) == moe.MOE_ERR_UNSUPPORTED
+    assert "scratch" in moe.last_error() and "1048576" in moe.last_error()
+    # the largest DeepSeek-V3 and skewed batches fit
+    for name in ("dsv3", "skewed", "mixtral", "k2decode"):
+        assert moe.workspace_size(wl.WORKLOADS[name].shape, moe.MOE_WS_PERMUTE) <= 1 << 20
+    # T = 0 is a no-op before any pointer is looked at
+    z = ctypes.byref(moe.shape_c(BASE.replace(T=0)))
+    assert L.moe_permute_noalloc(z, None, None, None, None, None, None, None, None) == moe.MOE_OK
