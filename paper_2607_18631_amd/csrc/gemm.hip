@@ -15,7 +15,8 @@
 // are copied global -> LDS by the direct-to-LDS loads of gfx950 (global_load_lds_dwordx4:
 // lane i of a wave instruction writes bytes [16 i, 16 i + 16) after the wave's LDS base),
 // issued STAGES-1 slices ahead, so HBM/L2 latency hides behind the MFMAs of the slices in
-// between and no VGPR staging is needed.  A slice is consumed after `s_waitcnt vmcnt`
+// between and no VGPR staging is needed; a slice's copies go out one per MFMA of the K-step
+// that follows the barrier that frees their ring slot.  A slice is consumed after `s_waitcnt vmcnt`
 // (this wave's copies of it have landed) and a workgroup barrier (everyone's have).
 // The barrier also orders the reuse of a ring slot: the slot refilled in iteration kt was
 // last read in iteration kt-1, which every wave has finished once it passes the barrier.
@@ -365,6 +366,29 @@ struct CopyPlan {
       dma16(reinterpret_cast<const bf16_t*>(wsb[j] + k0b + woff[j]), dst + BM * BK + (wave + NW * j) * 512);
   }
 
+  // Copy J of K slice kt into the ring slot at dst through a scalar base (the instruction's
+  // uniform row block plus the slice's byte offset) and the lane's 32-bit offset: no 64-bit
+  // per-lane address arithmetic and no per-lane 64-bit bases held across the K loop.  The
+  // compiler does not see these copies; the K loop orders them with its own vmcnt waits and
+  // barriers.
+  template <int J>
+  __device__ __forceinline__ void issue_one_sv(bf16_t* dst, int kt, int wave) const {
+    const int k0b = kt * BK * 2;
+    if constexpr (J < LX) {
+      dma16_sv(xbase + k0b, xoff[J], dst + (wave + NW * J) * 512);
+    } else {
+      constexpr int JW = J - LX;
+      dma16_sv(wsb[JW] + k0b, woff[JW], dst + BM * BK + (wave + NW * JW) * 512);
+    }
+  }
+  template <int J = 0>
+  __device__ __forceinline__ void issue_sv(bf16_t* dst, int kt, int wave) const {
+    if constexpr (J < L) {
+      issue_one_sv<J>(dst, kt, wave);
+      issue_sv<J + 1>(dst, kt, wave);
+    }
+  }
+
   // the partial last slice (K % BK != 0): chunks past K are fetched from K-8 and zeroed later
   __device__ __forceinline__ void issue_tail(bf16_t* dst, int kt, int wave, int K) const {
     const int k0 = kt * BK;
@@ -605,6 +629,23 @@ __device__ __forceinline__ void scatter_tile(const GemmProblem& p, const f32x16 
 }
 
 
+// One K-step's MFMAs with the next slice's copies between them: MFMA M (token fragment M / FN,
+// weight fragment M % FN) then copy M, while either remains.  Issuing a slice's copies in one
+// block held every wave's MFMA issue behind ~50 address and copy instructions right after the
+// slice barrier; spread this way the MFMA pipe keeps running (DeepSeek-V3 layer: up-projection
+// 945 -> 908 us, down-projection 510 -> 498 us; Mixtral -6 / -7%; skewed up-projection -8%).
+template <int M, int NA, int FN, int FM, int L, class CP>
+__device__ __forceinline__ void mfma_copy_steps(f32x16 (&acc)[FM][FN], const bf16x8 (&fw)[FN], const bf16x8 (&fx)[FM],
+                                                const CP& cp, bf16_t* dst, int kt, int wave) {
+  if constexpr (M < NA * FN || M < L) {
+    if constexpr (M < NA * FN)
+      acc[M / FN][M % FN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[M % FN], fx[M / FN], acc[M / FN][M % FN], 0, 0, 0);
+    if constexpr (M < L) cp.template issue_one_sv<M>(dst, kt, wave);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_copy_steps<M + 1, NA, FN, FM, L>(acc, fw, fx, cp, dst, kt, wave);
+  }
+}
+
 template <int FM, int FN>
 __device__ __forceinline__ void zero_acc(f32x16 (&acc)[FM][FN]) {
 #pragma unroll
@@ -657,21 +698,21 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       if (kt >= nk_full) cp.issue_tail(ring + st * SLICE, kt, wave, K);
       else cp.issue(ring + st * SLICE, kt, wave);
     } else {
-      cp.issue(ring + st * SLICE, kt, wave);
+      cp.issue_sv(ring + st * SLICE, kt, wave);
     }
   };
 
   // The current tile runs K slices kb .. kb + nl - 1; its i-th slice lives in ring slot
-  // i % STAGES.  sync_slice(i) makes slice i readable by every wave and refills the ring slot
-  // that slice i-1 used (i may be nl: then it only waits for every copy and synchronises).
+  // i % STAGES.  sync_slice(i) makes slice i readable by every wave and (issue) refills the ring
+  // slot that slice i-1 used (i may be nl: then it only waits for every copy and synchronises).
   int kb = 0, nl = nk;
-  auto sync_slice = [&](int i) {
+  auto sync_slice = [&](int i, bool issue = true) {
     const int after = min(STAGES - 2, nl - 1 - i);       // slices issued after i
     if (STAGES >= 4 && after >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * L : 0)>();
     else if (STAGES >= 3 && after >= 1) wait_vmcnt<(STAGES >= 3 ? L : 0)>();
     else wait_vmcnt<0>();
     lds_barrier();
-    if (i + STAGES - 1 < nl) issue_any(kb + i + STAGES - 1, (i + STAGES - 1) % STAGES);
+    if (issue && i + STAGES - 1 < nl) issue_any(kb + i + STAGES - 1, (i + STAGES - 1) % STAGES);
     const int kt = kb + i;
     if (ktail && i < nl && kt == nk - 1) {
       // zero the chunks past K of the last slice (their copies came from clamped addresses)
@@ -740,31 +781,65 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
       constexpr int NA = decltype(na)::value;
       sync_slice(0);
       load_frags(na, 0, 0, 0);
-      for (int i = 0; i < nl; ++i) {
+      // Slice i: K-steps 0 .. KS-2 read the next step's fragments during this step's MFMAs.  The
+      // last step's fragments are already in registers, so it first publishes slice i + 1 (vmcnt
+      // wait + barrier) and reads that slice's first fragments, then runs its MFMAs; with
+      // WITH_COPIES it also refills the ring slot slice i used (slice i + STAGES), one copy per
+      // MFMA.  After the final slice the fragment reads touch a stale ring slot, harmlessly, to
+      // keep the loop free of branches.  The slices that issue no copies run as a loop of their
+      // own: a uniform branch between the two MFMA sequences inside one loop body made the
+      // register allocator spill the accumulators.
+      auto slice_body = [&](int i, auto with_copies) {
+        constexpr bool WC = decltype(with_copies)::value;
         const int st = i % STAGES;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int cur = ks & 1;
           if (ks + 1 < KS) {
             load_frags(na, cur ^ 1, st, ks + 1);
-          } else {
-            // the last step's fragments are in registers: publish the next slice now, so the
-            // barrier and the first reads of the next slice overlap this step's MFMAs (after
-            // the final slice this reads a stale ring slot, harmlessly, to keep the loop
-            // free of branches the wait-count insertion would have to merge)
+#pragma unroll
+            for (int a = 0; a < NA; ++a)
+#pragma unroll
+              for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+            // scheduling: an MFMA first (its operands were read during the previous step), then
+            // the next step's LDS reads two at a time between MFMAs, so every read has several
+            // MFMAs of this step to hide its latency behind
+            if constexpr (NA > 0) sched_step<NA + FN, NA * FN>();
+          } else if constexpr (KTAIL) {
+            // K tail: the copies go out right after the barrier (the last slice's copies take
+            // clamped addresses and its chunks past K are zeroed inside sync_slice)
             sync_slice(i + 1);
             load_frags(na, cur ^ 1, (i + 1) % STAGES, 0);
+#pragma unroll
+            for (int a = 0; a < NA; ++a)
+#pragma unroll
+              for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+            if constexpr (NA > 0) sched_step<NA + FN, NA * FN>();
+          } else {
+            sync_slice(i + 1, false);
+            load_frags(na, cur ^ 1, (i + 1) % STAGES, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (WC) {
+              mfma_copy_steps<0, NA, FN, FM, L>(acc, fw[cur], fx[cur], cp, ring + st * SLICE, kb + i + STAGES, wave);
+            } else {
+#pragma unroll
+              for (int a = 0; a < NA; ++a)
+#pragma unroll
+                for (int b = 0; b < FN; ++b)
+                  acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
-#pragma unroll
-          for (int a = 0; a < NA; ++a)
-#pragma unroll
-            for (int b = 0; b < FN; ++b)
-              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][b], fx[cur][a], acc[a][b], 0, 0, 0);
-          // scheduling: an MFMA first (its operands were read during the previous step), then
-          // the next step's LDS reads two at a time between MFMAs, so every read has several
-          // MFMAs of this step to hide its latency behind
-          if constexpr (NA > 0) sched_step<NA + FN, NA * FN>();
         }
+      };
+      if constexpr (KTAIL) {
+        for (int i = 0; i < nl; ++i) slice_body(i, std::false_type{});
+      } else {
+        int i = 0;
+        for (; i < nl - STAGES; ++i) slice_body(i, std::true_type{});
+        for (; i < nl; ++i) slice_body(i, std::false_type{});
       }
     };
     const int live_blocks = min(BM / 32, (td.row_end - td.row0 + 31) / 32);

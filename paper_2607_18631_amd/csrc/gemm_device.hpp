@@ -23,12 +23,13 @@ __device__ __forceinline__ void dma16(const bf16_t* src, bf16_t* dst) {
 }
 
 // The same copy written as inline assembly, from a wave-uniform base `sbase` plus the lane's
-// 32-bit byte offset `voff`.  For kernels that read LDS with ds_read_b64_tr_b16: the compiler
-// makes every such read wait for all direct-to-LDS copies it knows of (vmcnt(0)), which would
-// serialise each slice's copies with the next slice's MFMAs.  Copies issued this way are
-// invisible to it; the kernel orders them itself (explicit vmcnt counts and barriers).  M0
-// carries the LDS address; kernels using this helper issue no compiler-generated LDS copies,
-// so nothing else of theirs keeps a value in M0.
+// 32-bit byte offset `voff`: no 64-bit per-lane address arithmetic per copy, and only the
+// 32-bit offsets stay live across a K loop.  Also for kernels that read LDS with
+// ds_read_b64_tr_b16: the compiler makes every such read wait for all direct-to-LDS copies it
+// knows of (vmcnt(0)), which would serialise each slice's copies with the next slice's MFMAs.
+// Copies issued this way are invisible to it; the kernel orders them itself (explicit vmcnt
+// counts and barriers).  M0 carries the LDS address; the asm declares M0 clobbered, so the
+// compiler keeps nothing of its own there across it.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16_sv(const char* sbase, uint32_t voff, bf16_t* dst) {
