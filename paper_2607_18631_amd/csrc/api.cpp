@@ -122,9 +122,7 @@ int check_ptr(const void* p, size_t align, const char* name) {
 size_t ws_route(const moe_shape_t* s) {
   return align_up((size_t)moe::logits_splits(s->T, s->E, s->d) * s->T * s->E * sizeof(float));
 }
-size_t ws_permute(const moe_shape_t* s) {
-  return 2 * align_up((size_t)moe::permute_blocks(s->T) * s->E_local * sizeof(int32_t));
-}
+size_t ws_permute(const moe_shape_t* s) { return moe::permute_ws(s->T, s->E_local).bytes; }
 size_t ws_ffn(const moe_shape_t* s) { return align_up((size_t)capacity(s) * s->F * sizeof(uint16_t)); }
 // backward: dA [cap, F], [dH dU] [cap, 2F], recomputed activation [cap, F] (bf16)
 size_t ws_ffn_bwd(const moe_shape_t* s) { return 4 * ws_ffn(s); }
@@ -313,8 +311,10 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
   p.expert_capacity = s->expert_capacity;
   p.topk_w = topk_w;
   p.row_weight = row_weight;
-  p.blk_count = static_cast<int32_t*>(ws);
-  p.blk_base = at<int32_t>(ws, ws_permute(s) / 2);
+  const moe::PermuteWs pw = moe::permute_ws(s->T, s->E_local);
+  p.super_count = at<int32_t>(ws, pw.super_count);
+  p.super_base = at<int32_t>(ws, pw.super_base);
+  p.totals = at<int32_t>(ws, pw.totals);
   return hip_status(moe::launch_permute(p, st, mark ? mark_permute : nullptr),
                     "permute launch");
 }

@@ -152,10 +152,16 @@ struct PermuteProblem {
   int32_t expert_capacity;    // > 0: masked-decode layout (rows e * C + rank, rank < C)
   const float* topk_w;        // [T, top_k]; read only when row_weight is set
   float* row_weight;          // [cap] gate of each row, or nullptr
-  int32_t* blk_count;         // workspace [nblk, E_local]
-  int32_t* blk_base;          // workspace [nblk, E_local]
+  int32_t* super_count;       // workspace [nsuper, E_local]: local slots per 512-token super-chunk
+  int32_t* super_base;        // workspace [nsuper, E_local]: their exclusive scan (wide tables only)
+  int32_t* totals;            // workspace [E_local]: expert totals (wide tables only)
 };
-int64_t permute_blocks(int64_t T);
+// super-chunks of T tokens, and the permutation workspace: byte offsets of its arrays and size
+int64_t permute_supers(int64_t T);
+struct PermuteWs {
+  size_t super_count, super_base, totals, bytes;
+};
+PermuteWs permute_ws(int64_t T, int E_local);
 // `between` (may be empty) runs on the host after the histogram launches and before the
 // permute launch (used to record a timing event between the two steps).
 hipError_t launch_permute(const PermuteProblem& p, hipStream_t stream, int (*between)() = nullptr);

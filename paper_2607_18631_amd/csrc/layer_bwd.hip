@@ -90,7 +90,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_combine_bwd(CombineBwdProblem p
     }
 #pragma unroll
     for (int a = 0; a < 16; ++a) {
-      if (a >= nact) break;
+      if (a >= nact) continue;                            // wave-uniform
       const bf16_t* yrow = p.y_perm + (int64_t)rows[a] * p.d;
       bf16_t* drow = p.dy_perm + (int64_t)rows[a] * p.d;
       u32x4 y[U];
@@ -120,9 +120,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_combine_bwd(CombineBwdProblem p
   }
 #pragma unroll
   for (int a = 0; a < 16; ++a) {
-    if (a >= nact) break;
-    const float s = wave_sum(part[a]);
-    if (lane == 0) p.dgate[t * k + s_slot[wv][a]] = s;
+    if (a < nact) {
+      const float s = wave_sum(part[a]);
+      if (lane == 0) p.dgate[t * k + s_slot[wv][a]] = s;
+    }
   }
 }
 

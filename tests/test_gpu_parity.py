@@ -43,6 +43,10 @@ SMALL = {
     # router logits on 256 x 256 tiles with a K split whose chunks are uneven: 110 slices of 64
     # (the last 24 wide) in 16 chunks of 7, the last chunk 5 slices
     "router_ksplit_ragged": (S(T=4096, d=7000, E=128, top_k=8, F=64, E_local=8, e_begin=40), None, 0.0),
+    # permutation count tables too wide for the placement kernel to scan itself (10 super-chunks of
+    # 512 tokens x 1024 experts; 79 super-chunks x 16 experts): the separate scan launch
+    "wide_count_table": (S(T=5000, d=64, E=1024, top_k=16, F=16, E_local=1024), None, 0.0),
+    "many_super_chunks": (S(T=40000, d=64, E=16, top_k=2, F=16, E_local=16), None, 0.0),
     # the kernel-crossover shape at expert multiplicities 4 and 32
     "crossover_me4": (wl.crossover(4).shape, None, 0.0),
     "crossover_me32": (wl.crossover(32).shape, None, 0.0),
