@@ -200,9 +200,9 @@ int moe_permute(const moe_shape_t* shape, const int32_t* topk_idx, const void* x
 /* moe_permute without a workspace argument, for callers that cannot allocate device memory
  * (code under HIP graph capture, serving loops that forbid allocation).  Same arguments,
  * results and layouts as moe_permute; its scratch (per-chunk counts and bases,
- * moe_workspace_size(shape, MOE_WS_PERMUTE) bytes, about 8 * ceil(T / 512) * E_local) lives in
+ * moe_workspace_size(shape, MOE_WS_PERMUTE) bytes, about 12 * ceil(T / 64) * E_local) lives in
  * a fixed 1 MiB device array owned by the library, one per device, kept until the process
- * ends.  Larger requests (e.g. E_local = 128 with T > 2^19) return MOE_ERR_UNSUPPORTED.  The call
+ * ends.  Larger requests (e.g. E_local = 128 with T > 43000) return MOE_ERR_UNSUPPORTED.  The call
  * allocates nothing; the first call on a device looks up the array's address there.
  * Every call on one GPU shares that GPU's array: calls that may overlap on one GPU (other
  * streams, other threads) race on it and must be ordered by the caller. */

@@ -315,6 +315,8 @@ int do_permute(const moe_shape_t* s, const int32_t* topk_idx, const void* x, int
   p.super_count = at<int32_t>(ws, pw.super_count);
   p.super_base = at<int32_t>(ws, pw.super_base);
   p.totals = at<int32_t>(ws, pw.totals);
+  p.chunk_mask = at<uint64_t>(ws, pw.chunk_mask);
+  p.chunk_base = at<int32_t>(ws, pw.chunk_base);
   return hip_status(moe::launch_permute(p, st, mark ? mark_permute : nullptr),
                     "permute launch");
 }

@@ -155,11 +155,13 @@ struct PermuteProblem {
   int32_t* super_count;       // workspace [nsuper, E_local]: local slots per 512-token super-chunk
   int32_t* super_base;        // workspace [nsuper, E_local]: their exclusive scan (wide tables only)
   int32_t* totals;            // workspace [E_local]: expert totals (wide tables only)
+  uint64_t* chunk_mask;       // workspace [nsuper * 8, E_local]: per 64-token chunk, lanes holding each expert
+  int32_t* chunk_base;        // workspace [nsuper * 8, E_local]: the chunk's base inside its super-chunk
 };
 // super-chunks of T tokens, and the permutation workspace: byte offsets of its arrays and size
 int64_t permute_supers(int64_t T);
 struct PermuteWs {
-  size_t super_count, super_base, totals, bytes;
+  size_t super_count, super_base, totals, chunk_mask, chunk_base, bytes;
 };
 PermuteWs permute_ws(int64_t T, int E_local);
 // `between` (may be empty) runs on the host after the histogram launches and before the

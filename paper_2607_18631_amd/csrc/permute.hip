@@ -2,28 +2,28 @@
 //
 // Tokens are cut into super-chunks of 512 (eight 64-token chunks, one wavefront each).  Two
 // launches (three for very wide count tables):
-//   k_super_rank  per super-chunk (one wave per chunk): each slot's rank among the
-//                 super-chunk's earlier slots of the same local expert (per chunk and expert, an
-//                 LDS mask of the lanes holding that expert: the popcount below the slot's lane;
-//                 then a scan of the eight chunks' counts), written to slot_row as a temporary,
-//                 and the super-chunk's count per local expert
+//   k_super_rank  per super-chunk (one wave per chunk): for every chunk and local expert, the
+//                 64-bit mask of the chunk's lanes (tokens) holding that expert and the chunk's
+//                 base inside the super-chunk (a scan of the eight chunks' counts), and the
+//                 super-chunk's count per local expert
 //   k_super_scan  (only when the super-chunk x expert count table is large) per expert, the
 //                 exclusive scan of the counts over super-chunks and the expert total
-//   k_place       per group of tokens of one super-chunk: the expert bases of that super-chunk
-//                 and the offsets (exclusive scan of the expert totals, the monotone
-//                 [E_local+1] array) from the count table, each slot's row
+//   k_place_*     per token: the expert bases of its super-chunk and the offsets (exclusive
+//                 scan of the expert totals, the monotone [E_local+1] array) from the count
+//                 table, each slot's rank (its chunk's base plus the popcount of its expert's
+//                 mask below its lane), hence its row
 //                     row = offsets[e] + base[super-chunk][e] + rank,
 //                 then slot_row / row_token (and the gate of each row when asked), counts and
-//                 offsets (first workgroup), and -- in the copy form, one wavefront per token --
-//                 the bit-exact copy of the token row to each of its local rows.  The copy form
-//                 issues the token row's loads before it reads the count table, so the table's
+//                 offsets (first workgroup), and -- in the copy forms, one wavefront per token --
+//                 the bit-exact copy of the token row to each of its local rows.  The copy forms
+//                 issue the token row's loads before they read the tables, so the tables'
 //                 latency hides behind them.
 //
 // Masked-decode layout (expert capacity C > 0): expert e's rows are e * C + rank for the
 // ranks below C; later slots are dropped (slot_row = -1) and offsets[e] = e * C.
 //
-// The in-chunk rank needs no ordering of atomics: each chunk's lane masks are the same whatever
-// order the ORs land in, so the order inside an expert is ascending token (a stable counting
+// The ranks need no ordering of atomics: each chunk's lane masks are the same whatever order
+// the LDS ORs land in, so the order inside an expert is ascending token (a stable counting
 // sort) and run-to-run identical.  Two slots of one token never share an expert, so a token
 // sets at most one bit of a mask.
 #include <mutex>
@@ -81,14 +81,21 @@ __global__ __launch_bounds__(64 * SCW) void k_super_rank(PermuteProblem p) {
     }
     p.super_count[(int64_t)s * E_local + e] = run;
   }
-  __syncthreads();
-  if (!valid_t) return;
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-#pragma unroll
-  for (int j = 0; j < 16; ++j)
-    if (j < k)
-      p.slot_row[t * k + j] =
-          myle[j] >= 0 ? s_base[w * E_local + myle[j]] + (int)__popcll(mask[myle[j]] & below) : -1;
+  __syncthreads();                             // every expert's bases written before they are stored
+  // the chunks' masks and bases inside the super-chunk, for the placement launch
+  for (int i = tid; i < SCW * E_local; i += 64 * SCW) {
+    const int64_t at = (int64_t)s * SCW * E_local + i;        // chunk s * SCW + i / E_local, expert i % E_local
+    p.chunk_mask[at] = s_mask[i];
+    p.chunk_base[at] = s_base[i];
+  }
+}
+
+// rank of token t's slot of local expert le among the earlier slots of le in t's super-chunk
+__device__ __forceinline__ int slot_rank(const PermuteProblem& p, int64_t t, int le) {
+  const int64_t at = (t / CH) * p.E_local + le;
+  const int pos = (int)(t % CH);
+  const uint64_t below = pos == 0 ? 0ull : (~0ull >> (64 - pos));
+  return p.chunk_base[at] + (int)__popcll(p.chunk_mask[at] & below);
 }
 
 // one workgroup per local expert: exclusive scan of super_count[:, e] over super-chunks, and
@@ -225,9 +232,9 @@ __global__ __launch_bounds__(64 * PT) void k_place_copy(PermuteProblem p, int ns
     le[j] = -1;
     srank[j] = -1;
     if (j < k && valid_t) {
-      srank[j] = p.slot_row[t * k + j];
       const int l = p.topk_idx[t * k + j] - p.e_begin;
-      le[j] = (l >= 0 && l < E_local && srank[j] >= 0) ? l : -1;
+      le[j] = (l >= 0 && l < E_local) ? l : -1;
+      if (le[j] >= 0) srank[j] = slot_rank(p, t, l);
       any |= le[j] >= 0;
     }
   }
@@ -283,11 +290,13 @@ __global__ __launch_bounds__(64 * PT) void k_place_copy(PermuteProblem p, int ns
 // q = g, g + NG, ... of expert e = l % EP, g = l / EP (EP = E_local rounded up to a power of two,
 // NG = 64 / EP lane groups); the groups' sums are combined by xor-shuffles and the totals scanned
 // within EP lanes.  `first` writes counts and offsets.
-__device__ __forceinline__ void wave_table(const PermuteProblem& p, int s, int nsuper, int ep, bool first, int& pre,
-                                           int& off) {
+// wave_table in two parts: the lane's sums over its super-chunks (issued first, as they depend on
+// nothing else), then the shuffles
+__device__ __forceinline__ void wave_table_sums(const PermuteProblem& p, int s, int nsuper, int ep, int& pre,
+                                                int& tot) {
   const int lane = threadIdx.x & 63, E_local = p.E_local;
   const int e = lane & (ep - 1), g = lane / ep, ng = 64 / ep;
-  int tot = 0;
+  tot = 0;
   pre = 0;
   if (e < E_local) {
 #pragma unroll 8
@@ -297,6 +306,11 @@ __device__ __forceinline__ void wave_table(const PermuteProblem& p, int s, int n
       tot += v;
     }
   }
+}
+__device__ __forceinline__ void wave_table_finish(const PermuteProblem& p, int ep, bool first, int& pre, int tot,
+                                                  int& off) {
+  const int lane = threadIdx.x & 63, E_local = p.E_local;
+  const int e = lane & (ep - 1);
   for (int o = ep; o < 64; o <<= 1) {
     pre += __shfl_xor(pre, o, 64);
     tot += __shfl_xor(tot, o, 64);
@@ -314,6 +328,12 @@ __device__ __forceinline__ void wave_table(const PermuteProblem& p, int s, int n
     if (lane == E_local - 1) p.offsets[E_local] = C > 0 ? E_local * C : inc;
   }
 }
+__device__ __forceinline__ void wave_table(const PermuteProblem& p, int s, int nsuper, int ep, bool first, int& pre,
+                                           int& off) {
+  int tot;
+  wave_table_sums(p, s, nsuper, ep, pre, tot);
+  wave_table_finish(p, ep, first, pre, tot, off);
+}
 
 // Copy form for up to 64 local experts and a count table of at most kInlineSupers super-chunks:
 // one wave per workgroup and token, the expert bases and offsets computed by the wave itself
@@ -325,6 +345,8 @@ __global__ __launch_bounds__(64) void k_place_wave(PermuteProblem p, int nsuper,
   const int k = p.top_k, E_local = p.E_local;
   const int64_t t = blockIdx.x;
   const int s = (int)(t / SC);
+  int pre, tot, off;
+  wave_table_sums(p, s, nsuper, ep, pre, tot);
   int le[16], srank[16];
   bool any = false;
 #pragma unroll
@@ -332,9 +354,9 @@ __global__ __launch_bounds__(64) void k_place_wave(PermuteProblem p, int nsuper,
     le[j] = -1;
     srank[j] = -1;
     if (j < k) {
-      srank[j] = p.slot_row[t * k + j];
       const int l = p.topk_idx[t * k + j] - p.e_begin;
-      le[j] = (l >= 0 && l < E_local && srank[j] >= 0) ? l : -1;
+      le[j] = (l >= 0 && l < E_local) ? l : -1;
+      if (le[j] >= 0) srank[j] = slot_rank(p, t, l);
       any |= le[j] >= 0;
     }
   }
@@ -348,8 +370,7 @@ __global__ __launch_bounds__(64) void k_place_wave(PermuteProblem p, int nsuper,
       if (v < nvec) val[u] = src[v];
     }
   }
-  int pre, off;
-  wave_table(p, s, nsuper, ep, t == 0, pre, off);
+  wave_table_finish(p, ep, t == 0, pre, tot, off);
   const int C = p.expert_capacity;
   int rows[16];
 #pragma unroll
@@ -388,7 +409,7 @@ __global__ __launch_bounds__(64) void k_place_wave(PermuteProblem p, int nsuper,
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int v = v0 + u * 64 + lane;
-        if (v < nvec) dst[v] = val[u];
+        if (v < nvec) __builtin_nontemporal_store(val[u], dst + v);   // streamed, not kept in the caches
       }
     }
   }
@@ -409,9 +430,9 @@ __global__ __launch_bounds__(64) void k_place_index_wave(PermuteProblem p, int n
     le[j] = -1;
     srank[j] = -1;
     if (j < k && valid_t) {
-      srank[j] = p.slot_row[t * k + j];
       const int l = p.topk_idx[t * k + j] - p.e_begin;
-      le[j] = (l >= 0 && l < E_local && srank[j] >= 0) ? l : -1;
+      le[j] = (l >= 0 && l < E_local) ? l : -1;
+      if (le[j] >= 0) srank[j] = slot_rank(p, t, l);
     }
   }
   int pre, off;
@@ -456,9 +477,9 @@ __global__ __launch_bounds__(PI) void k_place_index(PermuteProblem p, int nsuper
     le[j] = -1;
     srank[j] = -1;
     if (j < k && valid_t) {
-      srank[j] = p.slot_row[t * k + j];
       const int l = p.topk_idx[t * k + j] - p.e_begin;
-      le[j] = (l >= 0 && l < E_local && srank[j] >= 0) ? l : -1;
+      le[j] = (l >= 0 && l < E_local) ? l : -1;
+      if (le[j] >= 0) srank[j] = slot_rank(p, t, l);
     }
   }
   place_table(p, s, nsuper, scanned != 0, s_tab, s_tab + E_local, s_tab + 2 * E_local + 1, s_w);
@@ -523,10 +544,13 @@ PermuteWs permute_ws(int64_t T, int E_local) {
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   PermuteWs w;
   const size_t table = al((size_t)permute_supers(T) * E_local * sizeof(int32_t));
+  const size_t chunks = (size_t)permute_supers(T) * SCW * E_local;
   w.super_count = 0;
   w.super_base = table;
   w.totals = 2 * table;
-  w.bytes = 2 * table + al((size_t)E_local * sizeof(int32_t));
+  w.chunk_mask = w.totals + al((size_t)E_local * sizeof(int32_t));
+  w.chunk_base = w.chunk_mask + al(chunks * sizeof(uint64_t));
+  w.bytes = w.chunk_base + al(chunks * sizeof(int32_t));
   return w;
 }
 

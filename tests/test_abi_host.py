@@ -231,9 +231,9 @@ def test_permute_noalloc_validation():
     assert "slot_row" in moe.last_error()
     assert L.moe_permute_noalloc(sp, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == moe.MOE_ERR_INVALID_ARG
     assert "topk_idx is NULL" in moe.last_error()
-    # 512-token super-chunks x E_local counts and bases: T = 2^20 tokens over 128 local experts
-    # needs 2 MiB
-    big = BASE.replace(T=2 ** 20, E=128, E_local=128, top_k=8)
+    # per 64-token chunk and local expert a lane mask and a base (12 bytes): T = 2^16 tokens over
+    # 128 local experts needs 1.5 MiB
+    big = BASE.replace(T=2 ** 16, E=128, E_local=128, top_k=8)
     assert moe.workspace_size(big, moe.MOE_WS_PERMUTE) > 1 << 20
     assert L.moe_permute_noalloc(ctypes.byref(moe.shape_c(big)), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                  None) == moe.MOE_ERR_UNSUPPORTED
