@@ -11,9 +11,13 @@ top-8 sigmoid gating with 8 groups / top-4 groups, 32 local experts of width 204
 one shared expert of width 2048), the configuration the grouped-GEMM and HBM targets
 are quoted on.
 
-The dominant kernel's roofline figure uses per-step HIP events recorded by
-moe_layer_forward_traced inside the timed region; the CPU baseline times the fp64 oracle
-on a bounded sample of the same batch on the host cores.
+Timing follows the paper's kernel protocol on the timed steps: every step records HIP events
+between its launches (moe_layer_forward_traced, on the library's stream), and each figure is the
+median over 3 rounds of the per-round medians; the synchronised wall clock of the same steps is
+reported beside it.  The dominant kernel's roofline figure comes from those events; the CPU
+baseline times the fp64 oracle on a bounded sample of the same batch on the host cores.  The
+standalone permutation and combine are timed back to back, on the same buffers (warm: inputs
+partly in the 256 MB MALL) and rotating through buffer sets larger than the MALL (hbm).
 """
 from __future__ import annotations
 
@@ -119,6 +123,69 @@ def timed_median(fn, reps, rounds=3, warmup=10):
         torch.cuda.synchronize()
         meds.append(float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])))
     return float(np.median(meds))
+
+
+SCRUB_BYTES = 512 << 20          # read between calls for cold-cache figures (> the 256 MB MALL)
+ROTATE_BYTES = 768 << 20         # buffer sets rotated through for the HBM (cold) streaming figures
+
+
+class ReadProbe:
+    """libmoe_probe.so: a read-only stream kernel (the read ceiling, and the cache scrub of the
+    cold figures: reading leaves clean lines, so the next kernel pays no write-back)."""
+
+    def __init__(self):
+        import torch
+        from paper_2607_18631_amd import build as _b
+        self.lib = ctypes.CDLL(_b.PROBE_LIB)
+        self.lib.probe_read_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.probe_read_sink_words.restype = ctypes.c_int64
+        self.sink = torch.empty(int(self.lib.probe_read_sink_words()), dtype=torch.int32, device="cuda:0")
+
+    def read(self, buf):
+        import torch
+        st = torch.cuda.current_stream().cuda_stream
+        rc = self.lib.probe_read_stream(buf.data_ptr(), buf.numel() * buf.element_size(), self.sink.data_ptr(), st)
+        if rc != 0:
+            raise RuntimeError(f"probe_read_stream failed ({rc})")
+
+
+def back_to_back_ms(fn, calls, rounds=3, warmup=3):
+    """Median over `rounds` of the mean per-call time (ms) of `calls` calls issued back to back
+    between two events (no event between calls), after `warmup` calls."""
+    import numpy as np
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    res = []
+    for _ in range(rounds):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(calls):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res.append(e0.elapsed_time(e1) / calls)
+    return float(np.median(res))
+
+
+def cold_ms(fn, scrub, reps):
+    """Median time (ms) of one call of `fn` right after `scrub()` has streamed a buffer larger than
+    the MALL through the caches, so the call's inputs come from HBM; each call between two events."""
+    import numpy as np
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        scrub()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
 
 
 def crossover_run():
@@ -335,6 +402,7 @@ def all_workloads_run(steps):
     from paper_2607_18631_amd import moe
     from paper_2607_18631_amd import workloads as wl
     ev = HipEvents()
+    probe = ReadProbe()
     nstep = len(moe.MOE_STEP_NAMES)
     rows = []
     for name in wl.WORKLOADS:
@@ -343,6 +411,9 @@ def all_workloads_run(steps):
         sh = inputs["shape"]
         layer = moe.DeviceLayer(inputs, device="cuda:0")
         t = timed_median(layer.forward, steps)
+        scrub = torch.ones(SCRUB_BYTES, dtype=torch.uint8, device="cuda:0")
+        t_cold = cold_ms(layer.forward, lambda: probe.read(scrub), 20)
+        del scrub
         events = [ev.create(nstep + 1) for _ in range(steps)]
         for i in range(steps):
             layer.forward_traced(events[i])
@@ -367,10 +438,11 @@ def all_workloads_run(steps):
                      "gemm_us": float(gemm_ms * 1e3), "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
                      "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                      "layer_hbm_gbs": layer_bytes / (t * 1e-3) / 1e9,
+                     "layer_cold_us": t_cold * 1e3, "layer_hbm_gbs_cold": layer_bytes / (t_cold * 1e-3) / 1e9,
                      "layer_bound": bound, "layer_floor_us": floor_ms * 1e3,
                      "layer_frac_of_roofline": floor_ms / t,
                      "step_us": {n: round(float(split[i]) * 1e3, 2) for n, i in s.items()}})
-        log(f"{name}: {t * 1e3:.1f} us per layer, {rows[-1]['tokens_per_s']:.3g} tokens/s, "
+        log(f"{name}: {t * 1e3:.1f} us per layer ({t_cold * 1e3:.1f} cold), {rows[-1]['tokens_per_s']:.3g} tokens/s, "
             f"GEMM {rows[-1]['gemm_tflops']:.0f} TFLOP/s, {rows[-1]['layer_hbm_gbs']:.0f} GB/s")
         del layer, inputs
         torch.cuda.empty_cache()
@@ -495,7 +567,8 @@ def main():
                           "unit": "tokens/s", "higher_is_better": True, "n_gpus": 1, "dtype": "bf16",
                           "data": "synthetic", "vs_baseline": None,
                           "protocol": "warmup 10; median of 3 round medians of the per-call event times; step "
-                                      "split from traced calls",
+                                      "split from traced calls; cold = median of 20 calls each right after a "
+                                      "512 MiB read stream through the caches",
                           "peaks": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS},
                           "rows": rows}), flush=True)
         return
@@ -542,6 +615,8 @@ def main():
         layer.forward()
     torch.cuda.synchronize()
 
+    # exactly K timed steps, bracketed by synchronisations; each step records HIP events between
+    # its launches on the library's stream (moe_layer_forward_traced)
     events = [ev.create(nstep + 1) for _ in range(args.steps)]
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
@@ -551,13 +626,18 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per_step = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in events])  # ms
-    gpu_total = sum(ev.elapsed_ms(e[0], e[nstep]) for e in events)
+    per_call = np.array([ev.elapsed_ms(e[0], e[nstep]) for e in events])
     for e in events:
         ev.destroy(e)
-    ms_step = wall * 1e3 / args.steps
+    wall_ms_step = wall * 1e3 / args.steps
+    # the paper's protocol on the timed steps: median over 3 rounds of each round's median
+    rounds = np.array_split(np.arange(args.steps), min(3, args.steps))
+    mrm = lambda v: float(np.median([np.median(v[r]) for r in rounds]))
+    ms_step = mrm(per_call)
+    step_med = np.array([mrm(per_step[:, j]) for j in range(nstep)])
 
-    # standalone permutation (histogram, scan, ranks and the row copy), the form whose bytes
-    # the HBM figure counts; inside the layer the row copy is folded into the up-projection
+    # standalone permutation (rank, placement and row copy), the form whose bytes the HBM figure
+    # counts; inside the layer the row copy is folded into the up-projection
     log("timing the standalone permutation")
     T_, k_, cap_ = sh.T, sh.top_k, sh.capacity
     p_idx = layer.region(moe.MOE_REGION_TOPK_IDX, torch.int32, (T_, k_))
@@ -571,17 +651,41 @@ def main():
     def permute_once():
         moe.moe_permute(sh, p_idx, layer.x, p_counts, p_offsets, p_row_token, p_slot_row, p_x_perm, p_ws)
 
-    for _ in range(3):
-        permute_once()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 20
-    e0.record()
-    for _ in range(reps):
-        permute_once()
-    e1.record()
-    torch.cuda.synchronize()
-    permute_ms = e0.elapsed_time(e1) / reps
+    permute_ms = back_to_back_ms(permute_once, 50)
+    # from HBM: back to back over rotating copies of the token rows and outputs (> the MALL)
+    nrot = max(2, -(-ROTATE_BYTES // (2 * T_ * sh.d * 2)))
+    r_x = [layer.x.clone() for _ in range(nrot)]
+    r_xp = [torch.empty((cap_, sh.d), dtype=torch.bfloat16, device="cuda:0") for _ in range(nrot)]
+    rot = [0]
+
+    def permute_rot():
+        i = rot[0] = (rot[0] + 1) % nrot
+        moe.moe_permute(sh, p_idx, r_x[i], p_counts, p_offsets, p_row_token, p_slot_row, r_xp[i], p_ws)
+
+    permute_hbm_ms = back_to_back_ms(permute_rot, 48)
+    del r_x, r_xp
+
+    # standalone combine on the layer's expert rows (warm: back to back; cold: after a scrub)
+    log("timing the standalone combine")
+    c_y = layer.region(moe.MOE_REGION_Y_PERM, torch.bfloat16, (cap_, sh.d))
+    c_slot = layer.region(moe.MOE_REGION_SLOT_ROW, torch.int32, (T_, k_))
+    c_w = layer.region(moe.MOE_REGION_TOPK_W, torch.float32, (T_, k_))
+    c_sy = layer.region(moe.MOE_REGION_SHARED_Y, torch.bfloat16, (T_, sh.d)) if sh.F_shared > 0 else None
+    c_out = torch.empty((T_, sh.d), dtype=torch.bfloat16, device="cuda:0")
+    combine_once = lambda: moe.moe_combine(sh, c_y, c_slot, c_w, c_sy, c_out)
+    combine_b2b_ms = back_to_back_ms(combine_once, 50)
+    nrot_c = max(2, -(-ROTATE_BYTES // (3 * T_ * sh.d * 2)))
+    r_y = [c_y.clone() for _ in range(nrot_c)]
+    r_sy = [c_sy.clone() if c_sy is not None else None for _ in range(nrot_c)]
+    r_out = [torch.empty((T_, sh.d), dtype=torch.bfloat16, device="cuda:0") for _ in range(nrot_c)]
+    rot_c = [0]
+
+    def combine_rot():
+        i = rot_c[0] = (rot_c[0] + 1) % nrot_c
+        moe.moe_combine(sh, r_y[i], c_slot, c_w, r_sy[i], r_out[i])
+
+    combine_hbm_ms = back_to_back_ms(combine_rot, 48)
+    del c_out, r_y, r_sy, r_out
 
     # the routed experts alone (moe_grouped_ffn on the permuted rows, no shared expert): the
     # routed-only grouped-GEMM figure; the shape describes exactly the batch's local rows
@@ -597,11 +701,15 @@ def main():
         del r_y, r_ws
     del p_x_perm
 
-    # practical HBM ceiling: a plain 1 GiB device-to-device copy (bytes read + written per second)
-    log("timing a 1 GiB device copy")
+    # practical HBM ceilings on this part: a 1 GiB device copy (bytes read + written), a read-only
+    # stream (the probe kernel over 1 GiB) and a write-only stream (a 1 GiB fill)
+    log("timing 1 GiB copy, read and fill streams")
     c_src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda:0")
     c_dst = torch.empty_like(c_src)
     copy_ms = timed_median(lambda: c_dst.copy_(c_src), 10, warmup=3)
+    probe = ReadProbe()
+    read_ms = timed_median(lambda: probe.read(c_src), 10, warmup=3)
+    fill_ms = timed_median(lambda: c_dst.zero_(), 10, warmup=3)
     del c_src, c_dst
 
     # algorithmic work of this batch (from the routing the GPU produced)
@@ -614,13 +722,12 @@ def main():
     d, F, Fs, T, k = sh.d, sh.F, sh.F_shared, sh.T, sh.top_k
     up_flops = 4.0 * d * F * n_loc + 4.0 * d * Fs * T
     gemm_flops = 6.0 * d * F * n_loc + 6.0 * d * Fs * T
-    med = np.median(per_step, axis=0)
-    avg = per_step.mean(axis=0)
     s = {name: i for i, name in enumerate(moe.MOE_STEP_NAMES)}
-    up_ms = avg[s["ffn_up"]] + avg[s["shared_up"]]
+    up_ms = step_med[s["ffn_up"]] + step_med[s["shared_up"]]
+    up_avg_ms = per_step[:, s["ffn_up"]].mean() + per_step[:, s["shared_up"]].mean()
     # a shared expert as wide as the routed ones runs inside the routed launches
     up_launches = 2 if (Fs > 0 and Fs != F) else 1
-    gemm_ms = sum(avg[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
+    gemm_ms = sum(step_med[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
     perm_bytes = (tok_local + n_loc) * d * 2 + T * k * 8 + n_loc * 4
     comb_bytes = n_loc * d * 2 + (T * d * 2 if Fs > 0 else 0) + T * d * 2 + T * k * 8
     # whole-layer algorithmic HBM bytes (the decode-step figure): weights of the experts that
@@ -629,6 +736,7 @@ def main():
     layer_bytes = (active * 3 * d * F * 2 + 3 * d * Fs * 2 + sh.E * d * 2 + 2 * T * d * 2
                    + T * k * 8)
     achieved = up_flops / (up_ms * 1e-3) / 1e12
+    gbs = lambda by, ms: by / (ms * 1e-3) / 1e9
     res = {
         "metric": "MoE-layer tokens/s + grouped-GEMM TFLOP/s (% bf16 MFMA peak), 1 MI355X",
         "value": T / (ms_step * 1e-3),
@@ -645,19 +753,29 @@ def main():
         "config": {"workload": args.workload, "T": T, "d": d, "E": sh.E, "top_k": k, "E_local": sh.E_local,
                    "e_begin": sh.e_begin, "F": F, "F_shared": Fs, "gating": gating_desc(sh), "seed": inputs["seed"],
                    "local_rows": n_loc, "parallelism": "one expert-parallel rank's share on 1 GPU"},
+        "protocol": (f"warmup {args.warmup} steps, then exactly {args.steps} timed steps; ms_per_step and every "
+                     "step / kernel figure = median over 3 rounds of the per-step HIP-event medians; "
+                     "wall_ms_per_step = synchronised wall clock of the timed steps / steps"),
+        "wall_ms_per_step": wall_ms_step,
         "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
         "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         "routed_gemm_ms": routed_ms,
         "routed_gemm_tflops": (6.0 * d * F * n_loc / (routed_ms * 1e-3) / 1e12) if routed_ms else None,
-        "permute_gbs": perm_bytes / (permute_ms * 1e-3) / 1e9,
+        "permute_gbs": gbs(perm_bytes, permute_ms),
         "permute_ms": permute_ms,
+        "permute_hbm_gbs": gbs(perm_bytes, permute_hbm_ms),
         "permute_in_layer": "row copy folded into the up-projection (token rows read through row_token)",
-        "combine_gbs": comb_bytes / (avg[s["combine"]] * 1e-3) / 1e9,
+        "combine_gbs": gbs(comb_bytes, step_med[s["combine"]]),
+        "combine_b2b_gbs": gbs(comb_bytes, combine_b2b_ms),
+        "combine_hbm_gbs": gbs(comb_bytes, combine_hbm_ms),
+        "hbm_bytes": {"permute": perm_bytes, "combine": comb_bytes, "layer": layer_bytes},
         "copy_gbs": 2.0 * (1 << 30) / (copy_ms * 1e-3) / 1e9,
+        "read_gbs": (1 << 30) / (read_ms * 1e-3) / 1e9,
+        "fill_gbs": (1 << 30) / (fill_ms * 1e-3) / 1e9,
         "layer_hbm_gbs": layer_bytes / (ms_step * 1e-3) / 1e9,
         "active_local_experts": active,
-        "step_ms": {n: round(float(med[i]), 5) for n, i in s.items()},
-        "gpu_event_ms_per_step": gpu_total / args.steps,
+        "step_ms": {n: round(float(step_med[i]), 5) for n, i in s.items()},
+        "gpu_event_ms_per_step": float(per_call.mean()),
         "roofline": {
             "kernel": "k_grouped_gemm<EPI_SWIGLU> (W1/W3 GEMM + SwiGLU of the routed experts and the shared expert)",
             "bound": "mfma",
@@ -667,7 +785,8 @@ def main():
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": measured_traffic(args.workload),
             "launches_per_step": up_launches,
-            "avg_launch_ms": float(up_ms / up_launches),
+            "launch_ms": float(up_ms / up_launches),
+            "avg_launch_ms": float(up_avg_ms / up_launches),
             "flops_per_step": up_flops,
         },
     }

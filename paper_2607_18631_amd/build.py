@@ -17,6 +17,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmoe_mi355x.so")
+# bandwidth probes of the benchmark, a library of their own
+PROBE_SRC = os.path.join(HERE, "probe", "stream.hip")
+PROBE_LIB = os.path.join(HERE, "libmoe_probe.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "gemm.hip", "gemm_bwd.hip", "route.hip", "permute.hip", "combine.hip",
@@ -62,6 +65,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    _run([hipcc, *FLAGS, "-x", "hip", "-shared", PROBE_SRC, "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 
