@@ -22,7 +22,7 @@ PROBE_SRC = os.path.join(HERE, "probe", "stream.hip")
 PROBE_LIB = os.path.join(HERE, "libmoe_probe.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "gemm.hip", "gemm_bwd.hip", "route.hip", "permute.hip", "combine.hip",
+SOURCES = ["api.cpp", "sizes.cpp", "gemm.hip", "gemm_bwd.hip", "route.hip", "permute.hip", "combine.hip",
            "layer_bwd.hip"]
 
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

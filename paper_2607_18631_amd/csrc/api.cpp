@@ -1,7 +1,7 @@
 // C ABI of the MoE-layer forward: argument validation, workspace layout, kernel dispatch.
 // Every entry point validates on the host before touching the GPU, so an invalid call
 // returns its status without any HIP call; a valid call only enqueues work on `stream`.
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 
 #include <algorithm>
 #include <cmath>
@@ -912,7 +912,16 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     return fail(MOE_ERR_UNSUPPORTED, "E_local (%d) > %d", shape->E_local, moe::kMaxGroups);
   if (bias && shape->gate != MOE_GATE_SOFTMAX)
     return fail(MOE_ERR_UNSUPPORTED, "a router bias is only defined for softmax gating");
-  if (shape->T == 0) return ok();
+  if (events)
+    for (int i = 0; i <= MOE_STEP_COUNT_; ++i)
+      if (!events[i]) return fail(MOE_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  if (shape->T == 0) {
+    // nothing to compute; the events are still recorded, back to back (empty intervals)
+    if (events)
+      for (int i = 0; i <= MOE_STEP_COUNT_; ++i)
+        CHECK(hip_status(hipEventRecord(static_cast<hipEvent_t>(events[i]), as_stream(stream)), "hipEventRecord"));
+    return ok();
+  }
   CHECK(check_ptr(x, 16, "x"));
   CHECK(check_ptr(w_router, 16, "w_router"));
   if (bias) CHECK(check_ptr(bias, 4, "bias"));
@@ -927,9 +936,6 @@ int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void
     return fail(MOE_ERR_UNSUPPORTED, "MOE_FUSE_GATHER needs T * d * 2 (%lld) < 2^32",
                 (long long)(shape->T * (int64_t)shape->d * 2));
   CHECK(check_ws(shape, MOE_WS_LAYER, ws, ws_bytes));
-  if (events)
-    for (int i = 0; i <= MOE_STEP_COUNT_; ++i)
-      if (!events[i]) return fail(MOE_ERR_INVALID_ARG, "events[%d] is NULL", i);
 
   const LayerLayout L = layer_layout(shape);
   hipStream_t st = as_stream(stream);

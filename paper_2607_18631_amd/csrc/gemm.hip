@@ -54,34 +54,32 @@
 
 namespace moe {
 
-// device properties, queried once per device (concurrent first queries store the same values)
+// device properties, queried once per device (std::call_once on the first launch there)
 struct DevInfo {
-  std::atomic<int> cus{0};
-  std::atomic<int> lds{0};
+  std::once_flag once;
+  int cus = 256;
+  int lds = 65536;
 };
 static DevInfo g_dev[kMaxDevices];
 
-static DevInfo* dev_info() {
+static const DevInfo* dev_info() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
   DevInfo& d = g_dev[dev];
-  if (d.cus.load(std::memory_order_relaxed) == 0) {
+  std::call_once(d.once, [&] {
     int n = 0, l = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || l <= 0)
-      l = 65536;
-    d.lds.store(l, std::memory_order_relaxed);
-    d.cus.store(n, std::memory_order_relaxed);
-  }
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) d.cus = n;
+    if (hipDeviceGetAttribute(&l, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && l > 0) d.lds = l;
+  });
   return &d;
 }
 int cu_count() {
   const DevInfo* d = dev_info();
-  return d ? d->cus.load(std::memory_order_relaxed) : 256;
+  return d ? d->cus : 256;
 }
 int lds_limit() {
   const DevInfo* d = dev_info();
-  return d ? d->lds.load(std::memory_order_relaxed) : 65536;
+  return d ? d->lds : 65536;
 }
 
 int kernel_occupancy(OccCache& c, const void* fn, int nth, size_t lds, hipError_t& err) {
@@ -92,14 +90,15 @@ int kernel_occupancy(OccCache& c, const void* fn, int nth, size_t lds, hipError_
     err = hipErrorInvalidDevice;
     return 0;
   }
-  int v = c.per_cu[dev].load(std::memory_order_relaxed);
-  if (v > 0) return v;
-  if ((err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess) return 0;
-  int occ = 0;
-  if ((err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, nth, lds)) != hipSuccess) return 0;
-  v = occ > 0 ? occ : 1;
-  c.per_cu[dev].store(v, std::memory_order_relaxed);
-  return v;
+  std::call_once(c.once[dev], [&] {
+    int occ = 0;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, nth, lds);
+    c.err[dev] = e;
+    c.per_cu[dev] = occ > 0 ? occ : 1;
+  });
+  err = c.err[dev];
+  return err == hipSuccess ? c.per_cu[dev] : 0;
 }
 
 namespace {
@@ -956,47 +955,7 @@ hipError_t launch_cfg(int cfg, const GemmProblem& p, hipStream_t stream) {
 int g_force_cfg[3] = {-1, -1, -1};
 #endif
 
-// (BM, BN, BK) of the tile the fp32-output GEMM runs with: the 256 x 256 tile (K-split for
-// parallelism) when there are many tokens and experts, else 64 x 64 tiles
-struct TileShape {
-  int bm, bn, bk;
-};
-bool f32_big_tile(int64_t rows, int n) { return rows >= 4096 && n >= 128; }
-TileShape f32_tile(int64_t rows, int n) {
-#ifdef MOE_GEMM_SWEEP
-  switch (g_force_cfg[EPI_F32]) {
-    case 0: return {128, 128, 64};
-    case 6: return {256, 256, 64};
-    case 13: return {64, 64, 64};
-    case 14: return {64, 128, 64};
-    case 15: return {128, 64, 64};
-    case 16: return {32, 256, 64};
-    case 17: return {64, 256, 64};
-    case 18: return {128, 128, 64};
-    case 19: return {64, 64, 128};
-    default: break;
-  }
-#endif
-  if (f32_big_tile(rows, n)) return {256, 256, 64};
-  return {64, 64, 64};
-}
-
 }  // namespace
-
-int logits_splits(int64_t T, int E, int K) {
-  constexpr int64_t kTarget = 256;                         // compute units of an MI355X
-  constexpr int64_t kMaxSplits = 16;                       // bounds the partials the gate adds
-  const TileShape t = f32_tile(T, E);
-  const int64_t base = ((T + t.bm - 1) / t.bm) * ((E + t.bn - 1) / t.bn);
-  const int64_t nk = (K + t.bk - 1) / t.bk;
-  if (base <= 0 || nk <= 1) return 1;
-  int64_t s = (kTarget + base - 1) / base;
-  s = s < nk ? s : nk;
-  s = s < kMaxSplits ? s : kMaxSplits;
-  if (s <= 1) return 1;
-  const int64_t chunk = (nk + s - 1) / s;
-  return (int)((nk + chunk - 1) / chunk);                // every chunk non-empty
-}
 
 hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
   if (p.ksplit > 1 && (p.epi != EPI_F32 || p.offsets != nullptr || p.rows2 > 0)) return hipErrorInvalidValue;
@@ -1102,7 +1061,7 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
 #ifdef MOE_GEMM_SWEEP
       if (g_force_cfg[EPI_F32] >= 0) return launch_cfg<EPI_F32>(g_force_cfg[EPI_F32], p, stream);
 #endif
-      if (f32_big_tile(p.offsets ? p.max_rows : p.rows_single, p.N))
+      if (f32_tile(p.offsets ? p.max_rows : p.rows_single, p.N).bm == 256)
         return launch_tile<256, 256, 64, 2, 4, 2, EPI_F32>(p, stream);
       return launch_tile<64, 64, 64, 3, 2, 2, EPI_F32>(p, stream);
     default: return hipErrorInvalidValue;

@@ -1,9 +1,10 @@
-// Host-side launchers of the gfx950 kernels (internal to libmoe_mi355x.so).
+// Host-side launchers of the gfx950 kernels (internal to libmoe_mi355x.so), and the host-only
+// size arithmetic of their workspaces (sizes.cpp).
 #pragma once
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
-#include <atomic>
+#include <mutex>
 
 namespace moe {
 
@@ -76,12 +77,14 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream);
 int cu_count();
 int lds_limit();
 
-// Resident workgroups per CU of one kernel, cached per device: the first launch on a device
-// raises the kernel's dynamic-LDS limit to `lds` and queries the occupancy.  Concurrent first
-// launches compute and store the same value.  Returns 0 and sets err on failure.
+// Resident workgroups per CU of one kernel, per device: the first launch on a device raises the
+// kernel's dynamic-LDS limit to `lds` and queries the occupancy, once (std::call_once); later
+// launches read the stored result.  Returns 0 and sets err on failure.
 constexpr int kMaxDevices = 64;
 struct OccCache {
-  std::atomic<int> per_cu[kMaxDevices];
+  std::once_flag once[kMaxDevices];
+  int per_cu[kMaxDevices] = {};
+  hipError_t err[kMaxDevices] = {};
 };
 int kernel_occupancy(OccCache& c, const void* fn, int nth, size_t lds, hipError_t& err);
 
@@ -118,6 +121,13 @@ struct GemmBwdProblem {
   float* Yf;                  // BWD_KSEG: when set, float32 results here (same strides) instead of Y
 };
 hipError_t launch_gemm_bwd(const GemmBwdProblem& p, hipStream_t stream);
+
+// (BM, BN, BK) of the tile the fp32-output GEMM (router logits) runs with: the 256 x 256 tile
+// (K-split for parallelism) when there are many tokens and experts, else 64 x 64 tiles
+struct TileShape {
+  int bm, bn, bk;
+};
+TileShape f32_tile(int64_t rows, int n);
 
 // Number of K chunks the router-logits GEMM (T x E outputs, K = d) runs in: enough (m, n, k)
 // tiles for one per compute unit of the chip, every chunk non-empty.  Depends on the shape
@@ -158,6 +168,9 @@ struct PermuteProblem {
   uint64_t* chunk_mask;       // workspace [nsuper * 8, E_local]: per 64-token chunk, lanes holding each expert
   int32_t* chunk_base;        // workspace [nsuper * 8, E_local]: the chunk's base inside its super-chunk
 };
+// Permutation geometry: 64-token chunks (one wave), kPermSuper chunks per super-chunk.
+constexpr int kPermChunk = 64;
+constexpr int kPermSuper = 8;
 // super-chunks of T tokens, and the permutation workspace: byte offsets of its arrays and size
 int64_t permute_supers(int64_t T);
 struct PermuteWs {

@@ -34,8 +34,8 @@
 namespace moe {
 namespace {
 
-constexpr int CH = 64;           // tokens per chunk = lanes of one wave
-constexpr int SCW = 8;           // chunks (waves) per super-chunk
+constexpr int CH = kPermChunk;   // tokens per chunk = lanes of one wave
+constexpr int SCW = kPermSuper;  // chunks (waves) per super-chunk
 constexpr int SC = CH * SCW;     // tokens per super-chunk
 // count tables of at most this many super-chunks and entries (super-chunks x local experts) are
 // scanned by every k_place workgroup itself; larger ones by k_super_scan first
@@ -537,22 +537,6 @@ __global__ __launch_bounds__(256) void k_gather(PermuteProblem p) {
 }
 
 }  // namespace
-
-int64_t permute_supers(int64_t T) { return (T + SC - 1) / SC; }
-
-PermuteWs permute_ws(int64_t T, int E_local) {
-  auto al = [](size_t v) { return (v + 255) / 256 * 256; };
-  PermuteWs w;
-  const size_t table = al((size_t)permute_supers(T) * E_local * sizeof(int32_t));
-  const size_t chunks = (size_t)permute_supers(T) * SCW * E_local;
-  w.super_count = 0;
-  w.super_base = table;
-  w.totals = 2 * table;
-  w.chunk_mask = w.totals + al((size_t)E_local * sizeof(int32_t));
-  w.chunk_base = w.chunk_mask + al(chunks * sizeof(uint64_t));
-  w.bytes = w.chunk_base + al(chunks * sizeof(int32_t));
-  return w;
-}
 
 namespace {
 // k_super_rank's LDS (12 bytes per chunk and local expert) exceeds the default 64 KB dynamic limit
