@@ -175,7 +175,9 @@ size_t moe_workspace_size(const moe_shape_t* shape, int kind);
  * workspace.  Returns (size_t)-1 for an invalid shape or region. */
 size_t moe_workspace_offset(const moe_shape_t* shape, int region);
 
-/* Router logits, gating and top-k (steps 1-5 of the layer).
+/* Router logits, gating and top-k (steps 1-5 of the layer).  The paper states routing only in
+ * prose (Section 2, background: each token is routed to a small subset of experts); the gate
+ * formulas are the readings fixed by moe_gate_t and the group limit by n_group / topk_group.
  * Writes topk_idx and topk_w; when keys_out [T, E] f32 is not NULL it also receives
  * the float32 key every decision was taken on (softmax: logit + bias; sigmoid: the
  * sigmoid score), so a checker can replay the decision in the same precision.
@@ -184,7 +186,9 @@ int moe_route(const moe_shape_t* shape, const void* x, const void* w_router, con
               int32_t* topk_idx, float* topk_w, float* keys_out,
               void* ws, size_t ws_bytes, void* stream);
 
-/* Histogram, prefix scan and permutation (steps 6-8).
+/* Histogram, prefix scan and permutation (steps 6-8; Section 3.1, kernel spec: the token permute
+ * ahead of the grouped GEMM; Section 4, kernel generation: each expert's rows are the segment of
+ * a monotone [E+1] offset array, or the valid prefix of an equal-stride capacity segment).
  * From topk_idx, keeps the slots whose expert lies in [e_begin, e_begin + E_local),
  * writes counts and the monotone offsets (expert e owns rows [offsets[e], offsets[e+1])),
  * orders the rows of one expert by ascending token (a stable counting sort), writes
@@ -210,7 +214,10 @@ int moe_permute_noalloc(const moe_shape_t* shape, const int32_t* topk_idx, const
                         int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* slot_row,
                         void* x_perm, void* stream);
 
-/* Grouped SwiGLU expert MLP (step 9): for every local expert e and every row r in
+/* Grouped SwiGLU expert MLP (step 9; Section 4, engine registration: the forward composes the
+ * expert MLP's two GEMMs; Section 4, kernel generation: one kernel body reads each expert's rows
+ * through the offset array, or through capacity offsets plus valid counts in masked decode).
+ * For every local expert e and every row r in
  * [offsets[e], offsets[e+1]):  y_perm[r] = W2_e (silu(W1_e x_perm[r]) * (W3_e x_perm[r])).
  * The activation is rounded to bf16 before the second GEMM; accumulation is float32.
  * `offsets` is a device array of E_local + 1 entries (e.g. from moe_permute) and must
@@ -277,7 +284,8 @@ int moe_layer_backward(const moe_shape_t* shape, const void* x, const void* w_ro
                        void* dx, void* dw_router, void* dw13, void* dw2, void* dws13, void* dws2,
                        void* ws, size_t ws_bytes, void* stream);
 
-/* Gate-weighted combine (steps 10-11):
+/* Gate-weighted combine (steps 10-11; Section 3.1, kernel spec: the weighted combine after the
+ * grouped GEMM, or folded into its epilogue as fuse_combine):
  *   out[t] = bf16( sum over slots j with slot_row[t,j] >= 0 of topk_w[t,j] * y_perm[slot_row[t,j]]
  *                  + shared_y[t] )
  * accumulated in float32 in slot order, the shared row (NULL = none) added last, one

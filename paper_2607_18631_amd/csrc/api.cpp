@@ -283,6 +283,7 @@ int do_route(const moe_shape_t* s, const void* x, const void* w_router, const fl
   q.gate = s->gate;
   q.n_group = s->n_group;
   q.topk_group = s->topk_group;
+  q.group_size = s->E / s->n_group;
   q.renormalize = s->renormalize;
   q.routed_scale = s->routed_scale;
   q.topk_idx = topk_idx;

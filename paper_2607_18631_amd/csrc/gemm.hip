@@ -1061,9 +1061,12 @@ hipError_t launch_grouped_gemm(const GemmProblem& p, hipStream_t stream) {
 #ifdef MOE_GEMM_SWEEP
       if (g_force_cfg[EPI_F32] >= 0) return launch_cfg<EPI_F32>(g_force_cfg[EPI_F32], p, stream);
 #endif
-      if (f32_tile(p.offsets ? p.max_rows : p.rows_single, p.N).bm == 256)
-        return launch_tile<256, 256, 64, 2, 4, 2, EPI_F32>(p, stream);
+    {
+      const TileShape ft = f32_tile(p.offsets ? p.max_rows : p.rows_single, p.N);
+      if (ft.bn == 256) return launch_tile<128, 256, 64, 3, 2, 4, EPI_F32>(p, stream);
+      if (ft.bn == 128) return launch_tile<64, 128, 64, 3, 2, 2, EPI_F32>(p, stream);
       return launch_tile<64, 64, 64, 3, 2, 2, EPI_F32>(p, stream);
+    }
     default: return hipErrorInvalidValue;
   }
 }

@@ -141,6 +141,7 @@ struct GateProblem {
   const float* bias;          // [E] or nullptr
   int64_t T;
   int32_t E, top_k, gate, n_group, topk_group, renormalize;
+  int32_t group_size;         // E / n_group
   float routed_scale;
   int32_t* topk_idx;          // [T, top_k]
   float* topk_w;              // [T, top_k]

@@ -6,15 +6,17 @@
 // key (softmax: logit + bias; sigmoid: the score): the larger key wins, equal keys go to the
 // lower expert index, so the result does not depend on lane scheduling.
 //
-// Wave-wide argmax: a (key, index) pair is packed into one 64-bit integer whose unsigned
-// order is (key ascending, index descending), so the pair to keep is the plain maximum.  The
-// maximum is taken with DPP moves inside each 16-lane row (no LDS traffic) and four lane reads
-// across the rows.
+// Top-k, one expert per round: every key is mapped to a 32-bit unsigned integer with the same
+// order (chosen and ineligible experts map to 0, below every key), the wave maximum of the lanes'
+// largest values is taken with DPP moves (no LDS traffic), and of the lanes holding it the lowest
+// lane wins (a ballot), inside it the lowest expert: equal keys go to the lower expert index.
 //
-// Group limit (n_group > 1): the keys go through LDS; lane g scores group g (the float32 sum
-// of its two largest keys), ranks it against the other groups' scores (larger score first,
-// equal scores by lower group index), and a ballot of the ranks below topk_group is the mask
-// of eligible groups.
+// Group limit (n_group > 1): a group's score is the float32 sum of its two largest keys, and the
+// topk_group groups with the largest scores stay eligible (equal scores: lower group index first).
+// When each group is a run of 2, 4, 8 or 16 lanes, the scores come from DPP exchanges inside the
+// run and every lane ranks its own group against the others' scores read from their lanes;
+// otherwise the keys go through LDS, lane g scores and ranks group g, and a ballot of the ranks
+// below topk_group is the mask of eligible groups.
 #include <math.h>
 
 #include "common.hpp"
@@ -32,41 +34,27 @@ __device__ __forceinline__ uint32_t ordered(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ uint64_t pack_key(float key, int idx) {
-  return ((uint64_t)ordered(key) << 32) | (uint32_t)(~(uint32_t)idx);
-}
-__device__ __forceinline__ int packed_index(uint64_t v) { return (int)~(uint32_t)v; }
-// the float key back from a packed pair (inverse of ordered)
-__device__ __forceinline__ float packed_key(uint64_t v) {
-  const uint32_t o = (uint32_t)(v >> 32);
+// the float key back from its ordered image (inverse of ordered)
+__device__ __forceinline__ float unordered(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
 
-// lanes of the rows in ROWS take src from the DPP pattern CTRL, the others keep their value
+// lanes of the rows in ROWS take src from the DPP pattern CTRL, the others 0 (the identity of an
+// unsigned maximum, so each step below is one v_max_u32 with a DPP operand)
 template <int CTRL, int ROWS = 0xf>
-__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
-  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)v, (int)(uint32_t)v, CTRL, ROWS, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(v >> 32), (int)(uint32_t)(v >> 32), CTRL, ROWS, 0xf, false);
-  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-
-__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
-  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
-  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-  return ((uint64_t)hi << 32) | lo;
+__device__ __forceinline__ uint32_t dppu(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xf, false);
 }
 
 // maximum over the 64 lanes, returned to every lane (wave-uniform)
-__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
-  v = umax64(v, dpp64<0xb1>(v));          // quad_perm [1,0,3,2]
-  v = umax64(v, dpp64<0x4e>(v));          // quad_perm [2,3,0,1]
-  v = umax64(v, dpp64<0x141>(v));         // row_half_mirror: quads 0 <-> 1 of each 8
-  v = umax64(v, dpp64<0x140>(v));         // row_mirror: halves of each 16-lane row
-  v = umax64(v, dpp64<0x142, 0xa>(v));    // row_bcast:15 -> rows 1, 3 hold rows (0,1), (2,3)
-  v = umax64(v, dpp64<0x143, 0xc>(v));    // row_bcast:31 -> row 3 holds all four
-  return readlane64(v, 63);
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dppu<0xb1>(v));              // quad_perm [1,0,3,2]
+  v = max(v, dppu<0x4e>(v));              // quad_perm [2,3,0,1]
+  v = max(v, dppu<0x141>(v));             // row_half_mirror: quads 0 <-> 1 of each 8
+  v = max(v, dppu<0x140>(v));             // row_mirror: halves of each 16-lane row
+  v = max(v, dppu<0x142, 0xa>(v));        // row_bcast:15 -> rows 1, 3 hold rows (0,1), (2,3)
+  v = max(v, dppu<0x143, 0xc>(v));        // row_bcast:31 -> row 3 holds all four
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 template <int CTRL>
@@ -172,11 +160,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
   for (int j = 0; j < PL; ++j)
     if (e0 + j < E) elig |= 1u << j;
   if (p.n_group > 1) {
-    const int ng = p.n_group, gsz = E / ng;
+    const int ng = p.n_group, gsz = p.group_size;
     const int lpg = gsz / PL;                             // lanes per group when groups tile lanes
-    float gs = NEG;
     if (gsz % PL == 0 && (lpg == 2 || lpg == 4 || lpg == 8 || lpg == 16)) {
       // each group is a run of lpg lanes inside one 16-lane row: the two largest keys by DPP
+      // exchanges, after which every lane of the group holds the group's score
       float v1 = NEG, v2 = NEG;
 #pragma unroll
       for (int j = 0; j < PL; ++j) {
@@ -188,10 +176,17 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
       if (lpg >= 4) top2_merge<0x4e>(v1, v2);             // quads
       if (lpg >= 8) top2_merge<0x141>(v1, v2);            // 8 lanes
       if (lpg >= 16) top2_merge<0x140>(v1, v2);           // 16 lanes
-      if (lane % lpg == 0 && lane / lpg < ng) s_gscore[w][lane / lpg] = v1 + v2;
-      __builtin_amdgcn_wave_barrier();
-      if (lane < ng) gs = s_gscore[w][lane];
+      const float gs = v1 + v2;
+      const int sh = __builtin_ctz((unsigned)lpg);
+      const int g = lane >> sh;                           // this lane's group
+      int rank = 0;                                       // groups ahead of it
+      for (int h = 0; h < ng; ++h) {
+        const float o = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gs), h << sh));
+        rank += (o > gs || (o == gs && h < g)) ? 1 : 0;
+      }
+      if (rank >= p.topk_group) elig = 0;
     } else {
+      float gs = NEG;
 #pragma unroll
       for (int j = 0; j < PL; ++j) s_key[w][e0 + j] = key[j];
       __builtin_amdgcn_wave_barrier();
@@ -206,25 +201,31 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
         gs = v1 + v2;
         s_gscore[w][lane] = gs;
       }
-    }
-    __builtin_amdgcn_wave_barrier();
-    int rank = 0;
-    if (lane < ng)
+      __builtin_amdgcn_wave_barrier();
+      int rank = 0;
+      if (lane < ng)
 #pragma unroll 8
-      for (int h = 0; h < ng; ++h) {
-        const float o = s_gscore[w][h];
-        rank += (o > gs || (o == gs && h < lane)) ? 1 : 0;
-      }
-    const uint64_t keep = __ballot(lane < ng && rank < p.topk_group);
+        for (int h = 0; h < ng; ++h) {
+          const float o = s_gscore[w][h];
+          rank += (o > gs || (o == gs && h < lane)) ? 1 : 0;
+        }
+      const uint64_t keep = __ballot(lane < ng && rank < p.topk_group);
+      int g = e0 / gsz, r = e0 - g * gsz;                 // group of expert e0 + j, walked along j
 #pragma unroll
-    for (int j = 0; j < PL; ++j)
-      if (e0 + j < E && !((keep >> ((e0 + j) / gsz)) & 1ull)) elig &= ~(1u << j);
+      for (int j = 0; j < PL; ++j) {
+        if (e0 + j < E && !((keep >> g) & 1ull)) elig &= ~(1u << j);
+        if (++r == gsz) {
+          r = 0;
+          ++g;
+        }
+      }
+    }
   }
 
   // ---- top-k: k rounds of wave argmax over eligible, not yet chosen keys ----
-  uint64_t pk[PL];
+  uint32_t uk[PL];                                        // ordered keys; 0: not selectable
 #pragma unroll
-  for (int j = 0; j < PL; ++j) pk[j] = pack_key(key[j], e0 + j);
+  for (int j = 0; j < PL; ++j) uk[j] = ((elig >> j) & 1u) ? ordered(key[j]) : 0u;
   float selk[16];
   int seli[16];
 #pragma unroll
@@ -232,16 +233,21 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
     selk[r] = 0.f;
     seli[r] = 0;
     if (r < p.top_k) {
-      uint64_t best = 0;                                  // below every packed key
+      uint32_t best = uk[0];
 #pragma unroll
-      for (int j = 0; j < PL; ++j) best = umax64(best, ((elig >> j) & 1u) ? pk[j] : 0);
-      best = wave_max64(best);
-      // (the host guarantees at least top_k eligible experts, so best names one)
-      const int idx = min(max(packed_index(best), 0), E - 1);
-      seli[r] = idx;
-      selk[r] = packed_key(best);
-      const unsigned off = (unsigned)(idx - e0);
-      if (off < (unsigned)PL) elig &= ~(1u << off);
+      for (int j = 1; j < PL; ++j) best = max(best, uk[j]);
+      const uint32_t m = wave_max_u32(best);
+      // lowest lane holding the maximum (some lane does), then its lowest expert holding it
+      const int wl = __builtin_ctzll(__ballot(best == m));
+      int jf = PL - 1;
+#pragma unroll
+      for (int j = PL - 2; j >= 0; --j) jf = (uk[j] == m) ? j : jf;
+      const int jw = __builtin_amdgcn_readlane(jf, wl);
+      // (the host guarantees at least top_k eligible experts, so m names one)
+      seli[r] = min(wl * PL + jw, E - 1);
+      selk[r] = unordered(m);
+#pragma unroll
+      for (int j = 0; j < PL; ++j) uk[j] = (lane == wl && j == jw) ? 0u : uk[j];
     }
   }
 
@@ -274,8 +280,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
   float ow = 0.f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    oi = (lane == r) ? seli[r] : oi;
-    ow = (lane == r) ? wgt[r] : ow;
+    if (r < p.top_k) {
+      oi = (lane == r) ? seli[r] : oi;
+      ow = (lane == r) ? wgt[r] : ow;
+    }
   }
   ow = (divide ? ow / den : ow) * p.routed_scale;
   if (lane < p.top_k) {
