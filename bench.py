@@ -140,6 +140,11 @@ class ReadProbe:
         self.lib.probe_read_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         self.lib.probe_read_sink_words.restype = ctypes.c_int64
         self.sink = torch.empty(int(self.lib.probe_read_sink_words()), dtype=torch.int32, device="cuda:0")
+        self.lib.probe_mfma_loop.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.probe_mfma_blocks.restype = ctypes.c_int64
+        self.lib.probe_mfma_flops.argtypes = [ctypes.c_int]
+        self.lib.probe_mfma_flops.restype = ctypes.c_double
+        self.mfma_sink = None
 
     def read(self, buf):
         import torch
@@ -147,6 +152,17 @@ class ReadProbe:
         rc = self.lib.probe_read_stream(buf.data_ptr(), buf.numel() * buf.element_size(), self.sink.data_ptr(), st)
         if rc != 0:
             raise RuntimeError(f"probe_read_stream failed ({rc})")
+
+    def mfma(self, iters):
+        """One launch of the MFMA loop probe; returns its flops."""
+        import torch
+        if self.mfma_sink is None:
+            self.mfma_sink = torch.empty(int(self.lib.probe_mfma_blocks()) * 256, dtype=torch.float32,
+                                         device="cuda:0")
+        rc = self.lib.probe_mfma_loop(iters, self.mfma_sink.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"probe_mfma_loop failed ({rc})")
+        return self.lib.probe_mfma_flops(iters)
 
 
 def back_to_back_ms(fn, calls, rounds=3, warmup=3):
@@ -711,6 +727,12 @@ def main():
     read_ms = timed_median(lambda: probe.read(c_src), 10, warmup=3)
     fill_ms = timed_median(lambda: c_dst.zero_(), 10, warmup=3)
     del c_src, c_dst
+    # practical MFMA ceiling: independent bf16 MFMAs on register operands on every SIMD (2 waves
+    # each, as in the GEMM), a few ms per launch so that the clock settles under the load
+    log("timing the MFMA loop probe")
+    mfma_iters = 20000
+    mfma_ms = timed_median(lambda: probe.mfma(mfma_iters), 5, warmup=2)
+    mfma_tflops = probe.lib.probe_mfma_flops(mfma_iters) / (mfma_ms * 1e-3) / 1e12
 
     # algorithmic work of this batch (from the routing the GPU produced)
     offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
@@ -772,6 +794,8 @@ def main():
         "copy_gbs": 2.0 * (1 << 30) / (copy_ms * 1e-3) / 1e9,
         "read_gbs": (1 << 30) / (read_ms * 1e-3) / 1e9,
         "fill_gbs": (1 << 30) / (fill_ms * 1e-3) / 1e9,
+        "mfma_loop_tflops": mfma_tflops,
+        "mfma_loop_clock_ghz": mfma_tflops / PEAK_BF16_TFLOPS * 2.4,
         "layer_hbm_gbs": layer_bytes / (ms_step * 1e-3) / 1e9,
         "active_local_experts": active,
         "step_ms": {n: round(float(step_med[i]), 5) for n, i in s.items()},

@@ -1,11 +1,15 @@
-// Bandwidth probes of the benchmark (libmoe_probe.so, not part of the MoE library): a read-only
-// stream, the practical HBM read ceiling the layer's HBM-bound kernels are compared with.
+// Probes of the benchmark (libmoe_probe.so, not part of the MoE library): a read-only stream, the
+// practical HBM read ceiling the layer's HBM-bound kernels are compared with, and a loop of
+// independent bf16 MFMAs on register operands, the practical MFMA ceiling under full load (the
+// clock the part sustains with every matrix pipe busy, below the nominal 2.4 GHz).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Every lane reads 16-byte vectors at a grid stride, U in flight, and folds them with XOR; one
 // 4-byte store per wave keeps the loads alive.
@@ -27,6 +31,38 @@ __global__ __launch_bounds__(256) void k_read_stream(const u32x4* src, int64_t n
   if ((threadIdx.x & 63) == 0) sink[(blockIdx.x * blockDim.x + threadIdx.x) >> 6] = acc;
 }
 
+constexpr int kMfmaChains = 4;         // independent accumulators per wave
+constexpr int kMfmaBlocks = 256 * 2;   // two workgroups of 4 waves per compute unit (2 waves per SIMD)
+
+// Each wave issues iters x kMfmaChains v_mfma_f32_32x32x16_bf16 on fixed register operands (bf16
+// values from a hash of the lane, so the multipliers see varied data), then stores one float per
+// lane so that the loop is kept.
+__global__ __launch_bounds__(256) void k_mfma_loop(int iters, float* sink) {
+  const uint32_t lane = threadIdx.x;
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = (lane * 2654435761u) ^ (uint32_t)(i * 40503u);
+    a[i] = (__bf16)((float)((h >> 8) & 0xff) * (1.0f / 256.0f) - 0.5f);
+    b[i] = (__bf16)((float)((h >> 16) & 0xff) * (1.0f / 256.0f) - 0.5f);
+  }
+  f32x16 acc[kMfmaChains];
+#pragma unroll
+  for (int c = 0; c < kMfmaChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[c][i] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kMfmaChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float r = 0.f;
+#pragma unroll
+  for (int c = 0; c < kMfmaChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r += acc[c][i];
+  sink[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = r;
+}
+
 }  // namespace
 
 // Reads `bytes` (a multiple of 16) from the device buffer `src`; `sink` holds at least
@@ -40,3 +76,18 @@ extern "C" int probe_read_stream(const void* src, int64_t bytes, void* sink, voi
 }
 
 extern "C" int64_t probe_read_sink_words(void) { return 256 * 8 * 4; }
+
+// Runs the MFMA loop: probe_mfma_blocks() workgroups of 256 threads, each wave issuing iters x 4
+// MFMAs of 32 x 32 x 16 (32,768 flop each); `sink` holds probe_mfma_blocks() * 256 floats.
+// Returns a hipError_t.
+extern "C" int probe_mfma_loop(int iters, void* sink, void* stream) {
+  if (!sink || iters < 1) return (int)hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_mfma_loop, dim3(kMfmaBlocks), dim3(256), 0, reinterpret_cast<hipStream_t>(stream), iters,
+                     static_cast<float*>(sink));
+  return (int)hipGetLastError();
+}
+
+extern "C" int64_t probe_mfma_blocks(void) { return kMfmaBlocks; }
+
+// Flops of one probe_mfma_loop call.
+extern "C" double probe_mfma_flops(int iters) { return (double)kMfmaBlocks * 4 * iters * kMfmaChains * 32768.0; }
