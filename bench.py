@@ -631,9 +631,27 @@ def main():
         layer.forward()
     torch.cuda.synchronize()
 
-    # exactly K timed steps, bracketed by synchronisations; each step records HIP events between
-    # its launches on the library's stream (moe_layer_forward_traced)
-    events = [ev.create(nstep + 1) for _ in range(args.steps)]
+    # exactly K timed steps, bracketed by synchronisations.  Each recorded HIP event costs a few
+    # microseconds of GPU time, so a timed step records only three, on the library's stream
+    # (moe_layer_forward_traced with the other entries NULL): its start (the previous step's end)
+    # and the two around the SwiGLU up-projection, the kernel the roofline object reports; one more
+    # event closes the last step.
+    # (A shared expert narrower or wider than the routed ones has an up-projection launch of its
+    # own, bracketed the same way.)
+    up_steps = [moe.MOE_STEP_NAMES.index("ffn_up")]
+    if sh.F_shared > 0 and sh.F_shared != sh.F:
+        up_steps.append(moe.MOE_STEP_NAMES.index("shared_up"))
+    handles = [ev.create(1 + 2 * len(up_steps)) for _ in range(args.steps)]
+    end_ev = ev.create(1)
+    events = []
+    for i in range(args.steps):
+        arr = (ctypes.c_void_p * (nstep + 1))()
+        arr[0] = handles[i][0]
+        for u, j in enumerate(up_steps):
+            arr[j], arr[j + 1] = handles[i][1 + 2 * u], handles[i][2 + 2 * u]
+        if i == args.steps - 1:
+            arr[nstep] = end_ev[0]
+        events.append(arr)
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -641,15 +659,29 @@ def main():
         layer.forward_traced(events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_step = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in events])  # ms
-    per_call = np.array([ev.elapsed_ms(e[0], e[nstep]) for e in events])
-    for e in events:
-        ev.destroy(e)
+    starts = [h[0] for h in handles] + [end_ev[0]]
+    per_call = np.array([ev.elapsed_ms(starts[i], starts[i + 1]) for i in range(args.steps)])
+    up_call = np.array([sum(ev.elapsed_ms(h[1 + 2 * u], h[2 + 2 * u]) for u in range(len(up_steps)))
+                        for h in handles])
+    for h in handles:
+        ev.destroy(h)
+    ev.destroy(end_ev)
     wall_ms_step = wall * 1e3 / args.steps
     # the paper's protocol on the timed steps: median over 3 rounds of each round's median
     rounds = np.array_split(np.arange(args.steps), min(3, args.steps))
     mrm = lambda v: float(np.median([np.median(v[r]) for r in rounds]))
     ms_step = mrm(per_call)
+
+    # the split of a step into its launches, from separate fully traced steps after the timed ones
+    # (every step boundary recorded; these steps run ~35 us longer than untraced ones at DSv3)
+    log("tracing the step split")
+    tr_events = [ev.create(nstep + 1) for _ in range(args.steps)]
+    for i in range(args.steps):
+        layer.forward_traced(tr_events[i])
+    torch.cuda.synchronize()
+    per_step = np.array([[ev.elapsed_ms(e[j], e[j + 1]) for j in range(nstep)] for e in tr_events])  # ms
+    for e in tr_events:
+        ev.destroy(e)
     step_med = np.array([mrm(per_step[:, j]) for j in range(nstep)])
 
     # standalone permutation (rank, placement and row copy), the form whose bytes the HBM figure
@@ -745,10 +777,11 @@ def main():
     up_flops = 4.0 * d * F * n_loc + 4.0 * d * Fs * T
     gemm_flops = 6.0 * d * F * n_loc + 6.0 * d * Fs * T
     s = {name: i for i, name in enumerate(moe.MOE_STEP_NAMES)}
-    up_ms = step_med[s["ffn_up"]] + step_med[s["shared_up"]]
-    up_avg_ms = per_step[:, s["ffn_up"]].mean() + per_step[:, s["shared_up"]].mean()
-    # a shared expert as wide as the routed ones runs inside the routed launches
-    up_launches = 2 if (Fs > 0 and Fs != F) else 1
+    # up-projection launch time(s) from the timed steps; a shared expert as wide as the routed ones
+    # runs inside the routed launches
+    up_ms = mrm(up_call)
+    up_avg_ms = float(up_call.mean())
+    up_launches = len(up_steps)
     gemm_ms = sum(step_med[s[n]] for n in ("ffn_up", "ffn_down", "shared_up", "shared_down"))
     perm_bytes = (tok_local + n_loc) * d * 2 + T * k * 8 + n_loc * 4
     comb_bytes = n_loc * d * 2 + (T * d * 2 if Fs > 0 else 0) + T * d * 2 + T * k * 8
@@ -775,9 +808,11 @@ def main():
         "config": {"workload": args.workload, "T": T, "d": d, "E": sh.E, "top_k": k, "E_local": sh.E_local,
                    "e_begin": sh.e_begin, "F": F, "F_shared": Fs, "gating": gating_desc(sh), "seed": inputs["seed"],
                    "local_rows": n_loc, "parallelism": "one expert-parallel rank's share on 1 GPU"},
-        "protocol": (f"warmup {args.warmup} steps, then exactly {args.steps} timed steps; ms_per_step and every "
-                     "step / kernel figure = median over 3 rounds of the per-step HIP-event medians; "
-                     "wall_ms_per_step = synchronised wall clock of the timed steps / steps"),
+        "protocol": (f"warmup {args.warmup} steps, then exactly {args.steps} timed steps recording HIP events "
+                     "only at each step's start and around the up-projection launch; ms_per_step and the "
+                     "roofline launch time = median over 3 rounds of the per-step medians; "
+                     "wall_ms_per_step = synchronised wall clock of the timed steps / steps; step_ms from "
+                     "separately traced steps after the timed ones (every step boundary recorded)"),
         "wall_ms_per_step": wall_ms_step,
         "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
         "gemm_frac_of_bf16_peak": gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,

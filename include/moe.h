@@ -331,7 +331,9 @@ typedef enum moe_step {
  * MOE_STEP_COUNT_ + 1 hipEvent_t (as opaque pointers) created by the caller; events[i]
  * is recorded on `stream` right before step i is enqueued and events[MOE_STEP_COUNT_]
  * after the last step (a step that does not run gets its event recorded all the same,
- * so its interval is empty; with T == 0 every event is recorded, back to back).
+ * so its interval is empty; with T == 0 every event is recorded, back to back).  A NULL
+ * entry is not recorded: each recorded event adds a few microseconds of GPU time to the
+ * step, so a caller timing only some steps passes only their boundaries.
  * events == NULL behaves exactly like moe_layer_forward. */
 int moe_layer_forward_traced(const moe_shape_t* shape, const void* x, const void* w_router, const float* bias,
                              const void* w13, const void* w2, const void* ws13, const void* ws2,

@@ -183,7 +183,8 @@ def moe_layer_forward(sh, x, w_router, bias, w13, w2, ws13, ws2, out, ws, stream
 
 
 def moe_layer_forward_traced(sh, x, w_router, bias, w13, w2, ws13, ws2, out, ws, events, stream=None):
-    """``events``: ctypes array of len(MOE_STEP_NAMES) + 1 hipEvent_t handles (or None)."""
+    """``events``: ctypes array of len(MOE_STEP_NAMES) + 1 hipEvent_t handles (or None); a NULL
+    entry is not recorded."""
     _check(lib().moe_layer_forward_traced(ctypes.byref(shape_c(sh)), _p(x), _p(w_router), _p(bias), _p(w13),
                                           _p(w2), _p(ws13), _p(ws2), _p(out), _p(ws),
                                           0 if ws is None else ws.numel(), events, _stream(stream)))

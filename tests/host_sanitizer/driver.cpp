@@ -116,9 +116,11 @@ int main() {
   EXPECT(moe_layer_forward_traced(&z, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                   0, ev, nullptr) == MOE_OK && g_events - e0 == MOE_STEP_COUNT_ + 1,
          "T = 0 traced records %d events", g_events - e0);
-  ev[3] = nullptr;
+  ev[3] = nullptr;                                         // a NULL entry is skipped
+  const int e1 = g_events;
   EXPECT(moe_layer_forward_traced(&z, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                  0, ev, nullptr) == MOE_ERR_INVALID_ARG, "NULL event");
+                                  0, ev, nullptr) == MOE_OK && g_events - e1 == MOE_STEP_COUNT_,
+         "T = 0 traced with a NULL entry records %d events", g_events - e1);
   EXPECT(moe_permute_noalloc(&z, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr) == MOE_OK,
          "T = 0 noalloc");
 
@@ -165,6 +167,17 @@ int main() {
     EXPECT(sb == MOE_ERR_HIP, "workload %d backward reaches its first launch (status %d)", i, sb);
   }
   EXPECT(moe_permute_noalloc(&s, I, FAKE, I, I, I, I, FAKE, nullptr) == MOE_ERR_HIP, "noalloc scratch lookup");
+  {
+    // traced, only some events asked for: the first step's event is recorded, then its launch fails
+    void* sparse[MOE_STEP_COUNT_ + 1] = {};
+    sparse[0] = FAKE;
+    sparse[MOE_STEP_FFN_UP] = FAKE;
+    const size_t n = moe_workspace_size(&wl[2], MOE_WS_LAYER);
+    const int e2 = g_events;
+    const int st = moe_layer_forward_traced(&wl[2], FAKE, FAKE, nullptr, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, n,
+                                            sparse, nullptr);
+    EXPECT(st == MOE_ERR_HIP && g_events - e2 == 1, "sparse traced call (status %d, %d events)", st, g_events - e2);
+  }
 
   if (g_fail == 0) printf("ALL OK\n");
   return g_fail == 0 ? 0 : 1;
