@@ -127,14 +127,26 @@ __global__ __launch_bounds__(64 * kWaves) void k_gate(GateProblem p) {
   for (int j = 0; j < PL; ++j) key[j] = 0.f;
   const float* row0 = p.logits + t * E;
   int s = 0;
-  for (; s + 4 <= p.nsplit; s += 4) {                     // four partials' loads in flight
-    float v[4][PL];
+  // NB partials' loads in flight (NB * PL <= 64 registers), added in chunk order
+  constexpr int NB = PL <= 4 ? 8 : 64 / PL;
+  for (; s + NB <= p.nsplit; s += NB) {
+    float v[NB][PL];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) load_row(row0 + (s + u) * p.split_stride, v[u]);
+    for (int u = 0; u < NB; ++u) load_row(row0 + (s + u) * p.split_stride, v[u]);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < NB; ++u)
 #pragma unroll
       for (int j = 0; j < PL; ++j) key[j] += v[u][j];
+  }
+  if (s + NB / 2 <= p.nsplit) {
+    float v[NB / 2][PL];
+#pragma unroll
+    for (int u = 0; u < NB / 2; ++u) load_row(row0 + (s + u) * p.split_stride, v[u]);
+#pragma unroll
+    for (int u = 0; u < NB / 2; ++u)
+#pragma unroll
+      for (int j = 0; j < PL; ++j) key[j] += v[u][j];
+    s += NB / 2;
   }
   for (; s < p.nsplit; ++s) {
     float v[PL];
