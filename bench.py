@@ -371,6 +371,46 @@ def backward_run(workload, steps):
                 "backward_frac_of_bf16_peak": 16.0 * unit / (t_bwd * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
 
+def dense_ref_run(steps):
+    """The DeepSeek-V3-shaped shared expert (8192 tokens, d = 7168, F = 2048) as a dense MLP: the
+    library's grouped GEMMs on one group of 8192 rows (moe_grouped_ffn: W1/W3 + SwiGLU, then W2),
+    next to the vendor GEMM library on the same two products (torch.nn.functional.linear, i.e.
+    hipBLASLt; the SwiGLU between them is not timed).  A reference point for the grouped GEMM's
+    efficiency; profile it with rocprofv3 counters to compare the kernels."""
+    import torch
+    import torch.nn.functional as tf
+
+    from paper_2607_18631_amd import moe
+    from paper_2607_18631_amd import workloads as wl
+    inputs = wl.make_inputs("dsv3")
+    full = inputs["shape"]
+    T, d, F = full.T, full.d, full.F_shared
+    sh = wl.MoEShape(T=T, d=d, E=1, top_k=1, F=F, E_local=1)
+    dev = "cuda:0"
+    x = moe.to_device_bf16(inputs["x"], dev)
+    w13 = moe.to_device_bf16(inputs["ws13"], dev).reshape(1, 2 * F, d)
+    w2 = moe.to_device_bf16(inputs["ws2"], dev).reshape(1, d, F)
+    offsets = torch.tensor([0, T], dtype=torch.int32, device=dev)
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+    ws = moe.alloc_workspace(sh, moe.MOE_WS_FFN, dev)
+    t_ours = timed_median(lambda: moe.moe_grouped_ffn(sh, x, offsets, w13, w2, y, ws), steps)
+    w13_2d, w2_2d = w13[0], w2[0]
+    h = tf.linear(x, w13_2d)
+    act = (tf.silu(h[:, :F].float()) * h[:, F:].float()).to(torch.bfloat16)
+    t_up = timed_median(lambda: tf.linear(x, w13_2d), steps)
+    t_down = timed_median(lambda: tf.linear(act, w2_2d), steps)
+    ref = tf.linear(act, w2_2d).float()
+    err = float((y.float() - ref).norm() / ref.norm())
+    up_f, down_f = 4.0 * T * d * F, 2.0 * T * d * F
+    tfl = lambda f, ms: f / (ms * 1e-3) / 1e12
+    log(f"dense shared expert: library {t_ours * 1e3:.1f} us, vendor up {t_up * 1e3:.1f} + down {t_down * 1e3:.1f} us")
+    return {"T": T, "d": d, "F": F, "library_mlp_us": t_ours * 1e3, "library_mlp_tflops": tfl(up_f + down_f, t_ours),
+            "vendor_up_us": t_up * 1e3, "vendor_up_tflops": tfl(up_f, t_up),
+            "vendor_down_us": t_down * 1e3, "vendor_down_tflops": tfl(down_f, t_down),
+            "vendor_mlp_tflops": tfl(up_f + down_f, t_up + t_down),
+            "library_vs_vendor_rel_fro": err}
+
+
 def layer_backward_run(workload, steps):
     """The whole layer backward (moe_layer_backward) after one forward of the workload: per-call
     time (warmup 10, median of 3 round medians of `steps` calls) next to the forward's, and the
@@ -522,6 +562,8 @@ def main():
                     help="time the expert-MLP backward on one routed batch of --workload")
     ap.add_argument("--all-workloads", action="store_true",
                     help="time the layer on every workload (tiny, mixtral, dsv3, skewed, k2decode)")
+    ap.add_argument("--dense-ref", action="store_true",
+                    help="the DeepSeek-V3 shared expert as a dense MLP: the library's grouped GEMMs vs the vendor GEMM library")
     ap.add_argument("--layer-backward", action="store_true",
                     help="time the whole layer backward (moe_layer_backward) of --workload")
     ap.add_argument("--capacity", type=int, default=0,
@@ -587,6 +629,14 @@ def main():
                                       "512 MiB read stream through the caches",
                           "peaks": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS},
                           "rows": rows}), flush=True)
+        return
+    if args.dense_ref:
+        row = dense_ref_run(max(args.steps, 10))
+        print(json.dumps({"metric": "dense shared-expert MLP (DeepSeek-V3 shape): library grouped GEMMs vs vendor GEMM "
+                                    "library, 1 MI355X", "unit": "TFLOP/s", "higher_is_better": True, "n_gpus": 1,
+                          "dtype": "bf16", "data": "synthetic", "vs_baseline": None,
+                          "protocol": "warmup 10; median of 3 round medians of the per-call event times", **row}),
+              flush=True)
         return
     if args.layer_backward:
         sh, row = layer_backward_run(args.workload, max(args.steps, 10))
