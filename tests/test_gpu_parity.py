@@ -285,6 +285,20 @@ def test_full_workload_parity(name):
     full_layer_check(inputs, layer, out, name)
 
 
+@pytest.mark.parametrize("name,e_begin", [("dsv3", 224), ("k2decode", 336)])
+def test_full_workload_last_rank(name, e_begin):
+    """The full-size workload on the last expert-parallel rank's slice (DeepSeek-V3: experts
+    224-255, the last routing group; Kimi-K2 decode: experts 336-383): every token and every live
+    row against the oracle."""
+    print(f"[parity] full workload {name}, experts from {e_begin}: generating inputs", flush=True)
+    base = wl.make_inputs(name)
+    inputs = dict(base, shape=base["shape"].replace(e_begin=e_begin))
+    layer = moe.DeviceLayer(inputs)
+    out = layer.forward()
+    torch.cuda.synchronize()
+    full_layer_check(inputs, layer, out, f"{name} e_begin={e_begin}")
+
+
 @pytest.mark.parametrize("capacity", [2, 8, 64])
 def test_k2decode_masked_layout_full(capacity):
     """The masked-decode layout at the Kimi-K2 decode shape (T = 64, 48 of 384 experts local,
