@@ -313,6 +313,20 @@ def test_k2decode_masked_layout_full(capacity):
     full_layer_check(inputs, layer, out, f"k2decode masked C={capacity}")
 
 
+@pytest.mark.parametrize("capacity", [240, 320])
+def test_dsv3_masked_layout_full(capacity):
+    """The masked-decode layout at the DeepSeek-V3 size (32 local experts with 230-293 slots each):
+    C = 240 drops the slots ranked past 240 in most experts, C = 320 keeps every slot (its segments
+    fill the 320-row tiles the launch uses)."""
+    print(f"[parity] dsv3 masked C={capacity}: generating inputs", flush=True)
+    base = wl.make_inputs("dsv3")
+    inputs = dict(base, shape=base["shape"].replace(expert_capacity=capacity))
+    layer = moe.DeviceLayer(inputs)
+    out = layer.forward()
+    torch.cuda.synchronize()
+    full_layer_check(inputs, layer, out, f"dsv3 masked C={capacity}")
+
+
 def test_grouped_ffn_ragged_tail_blocks():
     """moe_grouped_ffn on hand-picked segment lengths: the last m-tile of a segment holds every
     count of live 32-row blocks (1 .. 8, block edges +-1), plus empty segments, multi-tile
