@@ -1,6 +1,6 @@
 """Benchmark of the MoE-layer forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload dsv3] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps 30] [--warmup 40] [--workload dsv3] [--no-cpu-baseline]
 
 One step = one moe_layer_forward (router logits, gating/top-k, histogram + scan,
 permutation, grouped SwiGLU expert MLP, shared expert, combine) over one batch of
@@ -105,14 +105,28 @@ def measured_traffic(workload):
     return float(fields["traffic_bytes_per_launch"])
 
 
+WARM_S = 0.1   # least busy time before any timed call: an idle part takes ~50 ms of load to reach its clock
+
+
+def warm_up(fn, calls):
+    """Batches of `calls` calls of `fn`, each batch synchronised, until at least WARM_S of wall time
+    has passed since the first call (at least one batch)."""
+    import torch
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(max(1, calls)):
+            fn()
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= WARM_S:
+            return
+
+
 def timed_median(fn, reps, rounds=3, warmup=10):
     """Median over `rounds` of the median per-call time (ms) of `reps` calls, each call between
-    two events on the current stream, after `warmup` calls."""
+    two events on the current stream, after `warmup` calls (more if they take under WARM_S)."""
     import numpy as np
     import torch
-    for _ in range(warmup):
-        fn()
-    torch.cuda.synchronize()
+    warm_up(fn, warmup)
     meds = []
     for _ in range(rounds):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
@@ -167,12 +181,11 @@ class ReadProbe:
 
 def back_to_back_ms(fn, calls, rounds=3, warmup=3):
     """Median over `rounds` of the mean per-call time (ms) of `calls` calls issued back to back
-    between two events (no event between calls), after `warmup` calls."""
+    between two events (no event between calls), after `warmup` calls (more if they take under
+    WARM_S)."""
     import numpy as np
     import torch
-    for _ in range(warmup):
-        fn()
-    torch.cuda.synchronize()
+    warm_up(fn, warmup)
     res = []
     for _ in range(rounds):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -208,7 +221,7 @@ def crossover_run():
     """The paper's RQ4 kernel-crossover workload: per-token latency over the global token count
     me * E / top_k, for the grouped expert MLP alone (exactly me rows per local expert, the
     figure's single-card expert compute) and for the whole layer on that many tokens.  Protocol:
-    warmup 10, 200 calls per round for me < 16 else 50, median of 3 round medians."""
+    warmup 10 calls and >= 0.1 s, 200 calls per round for me < 16 else 50, median of 3 round medians."""
     import numpy as np
     import torch
 
@@ -298,8 +311,8 @@ def masked_decode_run(workload, capacity):
 
 def fusion_matrix_run(workload, steps):
     """The layer in the paper's four kernel structures (fuse_gather x fuse_combine): per-call
-    time (warmup 10, median of 3 round medians of `steps` calls) and the per-step split of one
-    traced pass per call, averaged."""
+    time (warmup 10 calls and >= 0.1 s, median of 3 round medians of `steps` calls) and the
+    per-step split of one traced pass per call, averaged."""
     import numpy as np
     import torch
 
@@ -332,8 +345,8 @@ def fusion_matrix_run(workload, steps):
 def backward_run(workload, steps):
     """The expert-MLP backward (moe_grouped_ffn_backward) on the expert-ordered rows of one
     routed batch of the workload (its forward run unfused, so x_perm is materialised), next to
-    the forward expert MLP (moe_grouped_ffn) on the same rows.  Per-call times: warmup 10,
-    median of 3 round medians of `steps` calls."""
+    the forward expert MLP (moe_grouped_ffn) on the same rows.  Per-call times: warmup 10 calls
+    and >= 0.1 s, median of 3 round medians of `steps` calls."""
     import numpy as np
     import torch
 
@@ -413,9 +426,9 @@ def dense_ref_run(steps):
 
 def layer_backward_run(workload, steps):
     """The whole layer backward (moe_layer_backward) after one forward of the workload: per-call
-    time (warmup 10, median of 3 round medians of `steps` calls) next to the forward's, and the
-    executed MFMA work: expert and shared MLP backward 16 d F rows each (dA 2, recomputed
-    up-projection 4, dX 4, dW2 2, dW13 4), router 4 T E d (dx and dw_router)."""
+    time (warmup 10 calls and >= 0.1 s, median of 3 round medians of `steps` calls) next to the
+    forward's, and the executed MFMA work: expert and shared MLP backward 16 d F rows each (dA 2,
+    recomputed up-projection 4, dX 4, dW2 2, dW13 4), router 4 T E d (dx and dw_router)."""
     import numpy as np
     import torch
 
@@ -448,8 +461,8 @@ def layer_backward_run(workload, steps):
 
 
 def all_workloads_run(steps):
-    """Every workload of the metric's configuration list: per-call layer time (warmup 10, median of
-    3 round medians of `steps` calls), the per-step split from traced calls, tokens/s, the grouped
+    """Every workload of the metric's configuration list: per-call layer time (warmup 10 calls and
+    >= 0.1 s, median of 3 round medians of `steps` calls), the per-step split from traced calls, tokens/s, the grouped
     GEMMs' TFLOP/s, the layer's algorithmic HBM bytes per second, and the layer's roofline floor
     max(FLOPs / bf16 peak, bytes / HBM peak) as a fraction of the measured time."""
     import numpy as np
@@ -542,8 +555,9 @@ def cpu_baseline(inputs, sample_tokens):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=30)
+    # an idle part needs ~30-40 DeepSeek-V3-sized layer steps (~50 ms of load) to reach its clock
+    ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routed-gemm", action="store_true",
@@ -589,7 +603,7 @@ def main():
                                     "8 local experts), 1 MI355X",
                           "unit": "us/token", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
                           "data": "synthetic", "vs_baseline": None,
-                          "protocol": "warmup 10; 200 calls per round for me < 16 else 50; median of 3 round "
+                          "protocol": "warmup 10 calls and >= 0.1 s; 200 calls per round for me < 16 else 50; median of 3 round "
                                       "medians; HIP events on the library's stream",
                           "rows": rows}), flush=True)
         return
@@ -603,7 +617,7 @@ def main():
                           "config": {"workload": workload, "T": sh0.T, "d": sh0.d, "E": sh0.E, "top_k": sh0.top_k,
                                      "E_local": sh0.E_local, "F": sh0.F, "F_shared": sh0.F_shared,
                                      "expert_capacity": C},
-                          "protocol": "warmup 10; 50 calls per round; median of 3 round medians; HIP events on "
+                          "protocol": "warmup 10 calls and >= 0.1 s; 50 calls per round; median of 3 round medians; HIP events on "
                                       "the capturing stream",
                           "masked_equals_offsets_output": same,
                           "rows": rows}), flush=True)
@@ -615,7 +629,7 @@ def main():
                           "data": "synthetic", "vs_baseline": None,
                           "config": {"workload": args.workload, "T": sh.T, "d": sh.d, "E": sh.E, "top_k": sh.top_k,
                                      "E_local": sh.E_local, "F": sh.F},
-                          "protocol": "warmup 10; median of 3 round medians of the per-call event times",
+                          "protocol": "warmup 10 calls and >= 0.1 s; median of 3 round medians of the per-call event times",
                           **row}), flush=True)
         return
     if args.all_workloads:
@@ -624,7 +638,7 @@ def main():
                                     "1 MI355X",
                           "unit": "tokens/s", "higher_is_better": True, "n_gpus": 1, "dtype": "bf16",
                           "data": "synthetic", "vs_baseline": None,
-                          "protocol": "warmup 10; median of 3 round medians of the per-call event times; step "
+                          "protocol": "warmup 10 calls and >= 0.1 s; median of 3 round medians of the per-call event times; step "
                                       "split from traced calls; cold = median of 20 calls each right after a "
                                       "512 MiB read stream through the caches",
                           "peaks": {"bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS},
@@ -635,7 +649,7 @@ def main():
         print(json.dumps({"metric": "dense shared-expert MLP (DeepSeek-V3 shape): library grouped GEMMs vs vendor GEMM "
                                     "library, 1 MI355X", "unit": "TFLOP/s", "higher_is_better": True, "n_gpus": 1,
                           "dtype": "bf16", "data": "synthetic", "vs_baseline": None,
-                          "protocol": "warmup 10; median of 3 round medians of the per-call event times", **row}),
+                          "protocol": "warmup 10 calls and >= 0.1 s; median of 3 round medians of the per-call event times", **row}),
               flush=True)
         return
     if args.layer_backward:
@@ -646,7 +660,7 @@ def main():
                           "data": "synthetic", "vs_baseline": None,
                           "config": {"workload": args.workload, "T": sh.T, "d": sh.d, "E": sh.E, "top_k": sh.top_k,
                                      "E_local": sh.E_local, "F": sh.F, "F_shared": sh.F_shared},
-                          "protocol": "warmup 10; median of 3 round medians of the per-call event times",
+                          "protocol": "warmup 10 calls and >= 0.1 s; median of 3 round medians of the per-call event times",
                           **row}), flush=True)
         return
     if args.fusion_matrix:
@@ -657,7 +671,7 @@ def main():
                           "config": {"workload": args.workload, "T": sh0.T, "d": sh0.d, "E": sh0.E,
                                      "top_k": sh0.top_k, "E_local": sh0.E_local, "F": sh0.F,
                                      "F_shared": sh0.F_shared},
-                          "protocol": "warmup 10; median of 3 round medians of the per-call event times; step "
+                          "protocol": "warmup 10 calls and >= 0.1 s; median of 3 round medians of the per-call event times; step "
                                       "split from traced calls",
                           "rows": rows}), flush=True)
         return
