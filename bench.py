@@ -159,6 +159,11 @@ class ReadProbe:
         self.lib.probe_mfma_flops.argtypes = [ctypes.c_int]
         self.lib.probe_mfma_flops.restype = ctypes.c_double
         self.mfma_sink = None
+        self.lib.probe_lds_read.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.probe_lds_blocks.restype = ctypes.c_int64
+        self.lib.probe_lds_bytes.argtypes = [ctypes.c_int]
+        self.lib.probe_lds_bytes.restype = ctypes.c_double
+        self.lds_sink = self.lds_cycles = None
 
     def read(self, buf):
         import torch
@@ -177,6 +182,28 @@ class ReadProbe:
         if rc != 0:
             raise RuntimeError(f"probe_mfma_loop failed ({rc})")
         return self.lib.probe_mfma_flops(iters)
+
+    def lds(self, iters):
+        """One launch of the LDS read probe (two workgroups of 4 waves per CU); returns its bytes."""
+        import torch
+        if self.lds_sink is None:
+            nb = int(self.lib.probe_lds_blocks())
+            self.lds_sink = torch.empty(nb * 256, dtype=torch.int32, device="cuda:0")
+            self.lds_cycles = torch.empty(2 * nb, dtype=torch.int64, device="cuda:0")
+        rc = self.lib.probe_lds_read(iters, self.lds_sink.data_ptr(), self.lds_cycles.data_ptr(),
+                                     torch.cuda.current_stream().cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"probe_lds_read failed ({rc})")
+        return self.lib.probe_lds_bytes(iters)
+
+    def lds_clock_ghz(self):
+        """Shader clock (GHz) during the last probe_lds_read call: each workgroup's s_memtime cycles
+        over its 100 MHz s_memrealtime ticks (median)."""
+        import numpy as np
+        import torch
+        torch.cuda.synchronize()
+        c = self.lds_cycles.cpu().numpy().reshape(-1, 2).astype(np.float64)
+        return float(np.median(c[:, 0] / c[:, 1])) * 0.1
 
 
 def back_to_back_ms(fn, calls, rounds=3, warmup=3):
@@ -829,6 +856,12 @@ def main():
     mfma_iters = 20000
     mfma_ms = timed_median(lambda: probe.mfma(mfma_iters), 5, warmup=2)
     mfma_tflops = probe.lib.probe_mfma_flops(mfma_iters) / (mfma_ms * 1e-3) / 1e12
+    # LDS read ceiling: ds_read_b128 streams from LDS on every SIMD (2 waves each)
+    log("timing the LDS read probe")
+    lds_iters = 10000
+    lds_ms = timed_median(lambda: probe.lds(lds_iters), 5, warmup=2)
+    lds_tbs = probe.lib.probe_lds_bytes(lds_iters) / (lds_ms * 1e-3) / 1e12
+    lds_clock = probe.lds_clock_ghz()
 
     # algorithmic work of this batch (from the routing the GPU produced)
     offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
@@ -895,6 +928,9 @@ def main():
         "fill_gbs": (1 << 30) / (fill_ms * 1e-3) / 1e9,
         "mfma_loop_tflops": mfma_tflops,
         "mfma_loop_clock_ghz": mfma_tflops / PEAK_BF16_TFLOPS * 2.4,
+        "lds_read_tbs": lds_tbs,
+        "lds_read_bytes_per_clk_cu": lds_tbs * 1e12 / (256 * lds_clock * 1e9),
+        "lds_probe_clock_ghz": lds_clock,
         "layer_hbm_gbs": layer_bytes / (ms_step * 1e-3) / 1e9,
         "active_local_experts": active,
         "step_ms": {n: round(float(step_med[i]), 5) for n, i in s.items()},
