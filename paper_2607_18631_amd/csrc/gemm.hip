@@ -760,7 +760,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     }
   };
 
-  int tile = first_tile_slot();
+  // Round r of the persistent grid: the workgroup with first slot `slot` takes position
+  // r G + slot in even rounds and r G + (G - 1 - slot) in odd ones (a snake order).  Tiles of a
+  // routed expert cost in proportion to its live 32-row blocks; the snake pairs a workgroup's
+  // positions from opposite ends of the tile sequence, so the per-workgroup sums of 4 rounds
+  // scatter less.  An XCD still takes a contiguous block of positions in every round.
+  const int slot = first_tile_slot();
+  int round = 0;
+  int tile = slot;
   if (tile >= ts.total) return;
   TileDesc td = decode_tile<BM>(p, ts, tile);
   cp.setup(p, td, wave, lane);
@@ -847,7 +854,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
 
     // next tile: start its copies before this tile's epilogue (every wave is done with the ring)
     const TileDesc cur_td = td;
-    tile += G;
+    ++round;
+    tile = round * G + ((round & 1) ? G - 1 - slot : slot);
     const bool more = tile < ts.total;
     lds_barrier();
     if (more) {
