@@ -6,7 +6,8 @@
 // is [offsets[g], offsets[g+1]) -- the monotone [E+1] row-offset array of the paper's
 // kernel-generation section -- read from device memory, so the row counts never travel
 // to the host.  Each workgroup builds the launch's tile table in LDS (ceil(m_g / BM) x
-// n-tiles per group, one block-wide prefix sum) and then walks tiles persistently.
+// n-tiles per group, one block-wide prefix sum), decodes the tiles it will run into a short
+// list (one thread per tile), and then walks them persistently.
 // Tiles of one group are ordered m-fastest, so the m-tiles sharing a weight tile are
 // adjacent, and adjacent tiles go to workgroups of the same XCD (workgroup i runs on XCD
 // i mod 8): a weight tile is fetched from HBM once per XCD L2, not once per m-tile.
@@ -237,27 +238,28 @@ __device__ __forceinline__ void extra_position(const TileSpace& ts, int t, int& 
   x_before = min(S, first + (xblock ? o : 0));
 }
 
+// A tile's coordinates: rows [row0, row_end) of group g (-1: the extra group), output tile ni,
+// K slices [kb, ke) of K chunk kc.  Computed by any thread on its own (no wave-uniform input).
+struct TileCode {
+  int row0, row_end, ni, kb, ke, kc, g;
+};
+
 template <int BM>
-__device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const TileSpace& ts, int tile) {
-  TileDesc d;
-  d.kc = tile / ts.base_total;
-  tile -= d.kc * ts.base_total;
-  d.kb = d.kc * ts.kchunk;
-  d.ke = min(ts.nk, d.kb + ts.kchunk);
+__device__ __forceinline__ TileCode tile_code(const GemmProblem& p, const TileSpace& ts, int tile) {
+  TileCode c;
+  c.kc = tile / ts.base_total;
+  tile -= c.kc * ts.base_total;
+  c.kb = c.kc * ts.kchunk;
+  c.ke = min(ts.nk, c.kb + ts.kchunk);
   int x_before;
   bool extra;
   extra_position(ts, tile, x_before, extra);
   int row0g, local;
   if (extra) {
     row0g = 0;
-    d.row_end = p.rows2;
+    c.row_end = p.rows2;
     local = x_before;
-    d.W = p.W2;
-    d.X = p.X2;
-    d.Y = p.Y2;
-    d.rows = nullptr;
-    d.stok = nullptr;
-    d.sw = nullptr;
+    c.g = -1;
   } else {
     const int t = tile - x_before;                        // index among the grouped tiles
     int lo = 0, hi = ts.groups;                           // s_tp[groups] == grouped tiles > t
@@ -265,19 +267,13 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
       int mid = (lo + hi) >> 1;
       if (ts.s_tp[mid] <= t) lo = mid; else hi = mid;
     }
-    const int g = __builtin_amdgcn_readfirstlane(lo);
-    row0g = __builtin_amdgcn_readfirstlane(ts.seg_begin(g));
-    d.row_end = __builtin_amdgcn_readfirstlane(ts.seg_end(g));
-    local = t - __builtin_amdgcn_readfirstlane(ts.s_tp[g]);
-    d.W = p.W + (int64_t)g * p.w_group_stride;
-    d.X = p.X;
-    d.Y = p.Y;
-    d.rows = p.row_index;
-    d.stok = p.scatter_token;
-    d.sw = p.scatter_weight;
+    c.g = lo;
+    row0g = ts.seg_begin(lo);
+    c.row_end = ts.seg_end(lo);
+    local = t - ts.s_tp[lo];
   }
   const int bmg = extra ? ts.bmx : BM;                  // m-tile height of this group
-  const int mt = (d.row_end - row0g + bmg - 1) / bmg;
+  const int mt = (c.row_end - row0g + bmg - 1) / bmg;
   // banded order: bands of up to BAND_M m-tiles; inside a band m-fastest, then n.  The
   // 32 adjacent tiles one XCD runs at a time then share BAND_M token panels and
   // 32 / BAND_M weight panels (groups with few m-tiles reduce to plain m-fastest order)
@@ -286,10 +282,46 @@ __device__ __forceinline__ TileDesc decode_tile(const GemmProblem& p, const Tile
   const int bmt = min(BAND_M, mt - bm0);
   const int in_band = local - band * BAND_M * ts.tiles_n;
   const int mi = bm0 + in_band % bmt;
-  d.ni = in_band / bmt;
-  d.row0 = row0g + mi * bmg;
-  if (bmg < BM) d.row_end = min(d.row0 + bmg, d.row_end);   // the extra group's shorter tiles
+  c.ni = in_band / bmt;
+  c.row0 = row0g + mi * bmg;
+  if (bmg < BM) c.row_end = min(c.row0 + bmg, c.row_end);   // the extra group's shorter tiles
+  return c;
+}
+
+// The tile of a wave-uniform code (values moved to scalar registers) with its operand pointers.
+__device__ __forceinline__ TileDesc tile_desc(const GemmProblem& p, TileCode c) {
+  TileDesc d;
+  d.row0 = __builtin_amdgcn_readfirstlane(c.row0);
+  d.row_end = __builtin_amdgcn_readfirstlane(c.row_end);
+  d.ni = __builtin_amdgcn_readfirstlane(c.ni);
+  d.kb = __builtin_amdgcn_readfirstlane(c.kb);
+  d.ke = __builtin_amdgcn_readfirstlane(c.ke);
+  d.kc = __builtin_amdgcn_readfirstlane(c.kc);
+  const int g = __builtin_amdgcn_readfirstlane(c.g);
+  if (g < 0) {
+    d.W = p.W2;
+    d.X = p.X2;
+    d.Y = p.Y2;
+    d.rows = nullptr;
+    d.stok = nullptr;
+    d.sw = nullptr;
+  } else {
+    d.W = p.W + (int64_t)g * p.w_group_stride;
+    d.X = p.X;
+    d.Y = p.Y;
+    d.rows = p.row_index;
+    d.stok = p.scatter_token;
+    d.sw = p.scatter_weight;
+  }
   return d;
+}
+
+// Tiles a workgroup decodes once at its start (one thread per tile) and keeps in LDS; the
+// position of its round r is r G + slot in even rounds, r G + G - 1 - slot in odd ones.
+constexpr int kTileList = 64;
+__device__ __forceinline__ int round_position(int r, int slot) {
+  const int G = gridDim.x;
+  return r * G + ((r & 1) ? G - 1 - slot : slot);
 }
 
 // Copies of one K slice of a tile into a ring slot, spread over NW waves.  Per tile, a
@@ -680,6 +712,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   __shared__ int s_off[kMaxGroups + 1];
   __shared__ int s_tp[kMaxGroups + 1];
   __shared__ int s_tmp[NTH / 64];
+  __shared__ int s_list[kTileList][8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -769,7 +802,28 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
   int round = 0;
   int tile = slot;
   if (tile >= ts.total) return;
-  TileDesc td = decode_tile<BM>(p, ts, tile);
+  // this workgroup's tiles, decoded in parallel (the per-tile decode is ~2,500 cycles of integer
+  // divisions and an LDS binary search, on the critical path between two tiles)
+  for (int r = tid; r < kTileList; r += NTH) {
+    const int pos = round_position(r, slot);
+    if (pos < ts.total) {
+      const TileCode c = tile_code<BM>(p, ts, pos);
+      s_list[r][0] = c.row0; s_list[r][1] = c.row_end; s_list[r][2] = c.ni; s_list[r][3] = c.kb;
+      s_list[r][4] = c.ke; s_list[r][5] = c.kc; s_list[r][6] = c.g;
+    }
+  }
+  __syncthreads();
+  auto fetch_tile = [&](int r, int pos) -> TileDesc {
+    TileCode c;
+    if (r < kTileList) {
+      c.row0 = s_list[r][0]; c.row_end = s_list[r][1]; c.ni = s_list[r][2]; c.kb = s_list[r][3];
+      c.ke = s_list[r][4]; c.kc = s_list[r][5]; c.g = s_list[r][6];
+    } else {
+      c = tile_code<BM>(p, ts, pos);
+    }
+    return tile_desc(p, c);
+  };
+  TileDesc td = fetch_tile(0, tile);
   cp.setup(p, td, wave, lane);
   kb = td.kb;
   nl = td.ke - td.kb;
@@ -855,11 +909,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
     // next tile: start its copies before this tile's epilogue (every wave is done with the ring)
     const TileDesc cur_td = td;
     ++round;
-    tile = round * G + ((round & 1) ? G - 1 - slot : slot);
+    tile = round_position(round, slot);
     const bool more = tile < ts.total;
     lds_barrier();
     if (more) {
-      td = decode_tile<BM>(p, ts, tile);
+      td = fetch_tile(round, tile);
       cp.setup(p, td, wave, lane);
       kb = td.kb;
       nl = td.ke - td.kb;
@@ -891,7 +945,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void k_grouped_gemm(GemmProblem 
 // down to whole rounds of the 8 XCDs.  `occ` caches the kernel's occupancy per device.
 hipError_t launch_persistent(const void* fn, OccCache& occ, int nth, size_t lds, int bm, int outn,
                              const GemmProblem& p, hipStream_t stream) {
-  const size_t lds_static = 2 * (kMaxGroups + 1) * sizeof(int) + 64;
+  const size_t lds_static = 2 * (kMaxGroups + 1) * sizeof(int) + kTileList * 8 * sizeof(int) + 64;
   if (lds + lds_static > (size_t)lds_limit()) return hipErrorInvalidConfiguration;
   hipError_t err;
   const int per_cu = kernel_occupancy(occ, fn, nth, lds, err);
