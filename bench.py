@@ -715,6 +715,30 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    # The part's ceilings, measured before the layer (their ~0.5 s of load also brings an idle part
+    # to its steady clock ahead of the warmup steps).  HBM: a 1 GiB device copy (bytes read +
+    # written), a read-only stream (the probe kernel over 1 GiB) and a write-only stream (a 1 GiB fill)
+    log("timing 1 GiB copy, read and fill streams")
+    c_src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda:0")
+    c_dst = torch.empty_like(c_src)
+    copy_ms = timed_median(lambda: c_dst.copy_(c_src), 10, warmup=3)
+    probe = ReadProbe()
+    read_ms = timed_median(lambda: probe.read(c_src), 10, warmup=3)
+    fill_ms = timed_median(lambda: c_dst.zero_(), 10, warmup=3)
+    del c_src, c_dst
+    # practical MFMA ceiling: independent bf16 MFMAs on register operands on every SIMD (2 waves
+    # each, as in the GEMM), a few ms per launch so that the clock settles under the load
+    log("timing the MFMA loop probe")
+    mfma_iters = 20000
+    mfma_ms = timed_median(lambda: probe.mfma(mfma_iters), 5, warmup=2)
+    mfma_tflops = probe.lib.probe_mfma_flops(mfma_iters) / (mfma_ms * 1e-3) / 1e12
+    # LDS read ceiling: ds_read_b128 streams from LDS on every SIMD (2 waves each)
+    log("timing the LDS read probe")
+    lds_iters = 10000
+    lds_ms = timed_median(lambda: probe.lds(lds_iters), 5, warmup=2)
+    lds_tbs = probe.lib.probe_lds_bytes(lds_iters) / (lds_ms * 1e-3) / 1e12
+    lds_clock = probe.lds_clock_ghz()
+
     ev = HipEvents()
     nstep = len(moe.MOE_STEP_NAMES)
     log(f"warmup {args.warmup} steps")
@@ -839,29 +863,6 @@ def main():
                                                              r_ws), 20)
         del r_y, r_ws
     del p_x_perm
-
-    # practical HBM ceilings on this part: a 1 GiB device copy (bytes read + written), a read-only
-    # stream (the probe kernel over 1 GiB) and a write-only stream (a 1 GiB fill)
-    log("timing 1 GiB copy, read and fill streams")
-    c_src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda:0")
-    c_dst = torch.empty_like(c_src)
-    copy_ms = timed_median(lambda: c_dst.copy_(c_src), 10, warmup=3)
-    probe = ReadProbe()
-    read_ms = timed_median(lambda: probe.read(c_src), 10, warmup=3)
-    fill_ms = timed_median(lambda: c_dst.zero_(), 10, warmup=3)
-    del c_src, c_dst
-    # practical MFMA ceiling: independent bf16 MFMAs on register operands on every SIMD (2 waves
-    # each, as in the GEMM), a few ms per launch so that the clock settles under the load
-    log("timing the MFMA loop probe")
-    mfma_iters = 20000
-    mfma_ms = timed_median(lambda: probe.mfma(mfma_iters), 5, warmup=2)
-    mfma_tflops = probe.lib.probe_mfma_flops(mfma_iters) / (mfma_ms * 1e-3) / 1e12
-    # LDS read ceiling: ds_read_b128 streams from LDS on every SIMD (2 waves each)
-    log("timing the LDS read probe")
-    lds_iters = 10000
-    lds_ms = timed_median(lambda: probe.lds(lds_iters), 5, warmup=2)
-    lds_tbs = probe.lib.probe_lds_bytes(lds_iters) / (lds_ms * 1e-3) / 1e12
-    lds_clock = probe.lds_clock_ghz()
 
     # algorithmic work of this batch (from the routing the GPU produced)
     offsets = layer.region(moe.MOE_REGION_OFFSETS, torch.int32, (sh.E_local + 1,)).cpu().numpy()
