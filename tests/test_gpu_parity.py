@@ -357,6 +357,43 @@ def test_grouped_ffn_ragged_tail_blocks():
         assert err <= REL_TOL, (e, lengths[e], err)
 
 
+def test_grouped_ffn_more_rounds_than_the_tile_list():
+    """moe_grouped_ffn with 1024 groups of 60..140 rows and d = 2048: the down-projection launch
+    has more than 64 rounds of tiles per workgroup even at two workgroups per CU, so the tiles past
+    a workgroup's 64-entry LDS tile list are decoded on the fly.  The first groups, a spread of
+    middle ones and all of the last ones (whose tiles come last) against the oracle.  Inputs from
+    torch's seeded GPU generator (0.6 G values); the checked groups are copied back for the oracle."""
+    E, d, F = 1024, 2048, 64
+    rng = np.random.default_rng(77)
+    lengths = rng.integers(60, 141, size=E)
+    T = int(lengths.sum())
+    sh = S(T=T, d=d, E=E, top_k=1, F=F, E_local=E)
+    # at most two workgroups per CU on 256 CUs, 64-row tiles, 128-wide output tiles
+    tiles_down = int(sum((l + 63) // 64 for l in lengths)) * (d // 128)
+    assert tiles_down > 64 * 512, tiles_down
+    dev = "cuda"
+    g = torch.Generator(device=dev).manual_seed(77)
+    x = torch.randn(T, d, device=dev, generator=g).bfloat16()
+    w13 = (torch.randn(E, 2 * F, d, device=dev, generator=g) * d ** -0.5).bfloat16()
+    w2 = (torch.randn(E, d, F, device=dev, generator=g) * F ** -0.5).bfloat16()
+    offs = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    y = torch.full((sh.capacity, d), float("nan"), dtype=torch.bfloat16, device=dev)
+    moe.moe_grouped_ffn(sh, x, torch.from_numpy(offs).to(dev), w13, w2, y, moe.alloc_workspace(sh, moe.MOE_WS_FFN))
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(y[:T].float()).all())
+    check = list(range(4)) + list(range(100, E - 64, 97)) + list(range(E - 64, E))
+    worst = 0.0
+    for e in check:
+        a, b = int(offs[e]), int(offs[e + 1])
+        ref = oracle.swiglu_ffn(oracle.bf16_to_f64(dev_bits(x[a:b])), oracle.bf16_to_f64(dev_bits(w13[e])),
+                                oracle.bf16_to_f64(dev_bits(w2[e])))
+        err = rel_fro(oracle.bf16_to_f64(dev_bits(y[a:b])), ref)
+        worst = max(worst, err)
+        assert err <= REL_TOL, (e, b - a, err)
+    print(f"[parity] grouped_ffn {E} groups, {tiles_down} down-projection tiles: worst rel_fro {worst:.3e} "
+          f"over {len(check)} groups", flush=True)
+
+
 def test_library_loaded_before_torch():
     """The binding loaded before anything imported torch (a fresh process) still runs the layer:
     the library must bind to the HIP runtime torch uses, not to a second copy of it."""
