@@ -244,3 +244,21 @@ def test_permute_noalloc_validation():
     # T = 0 is a no-op before any pointer is looked at
     z = ctypes.byref(moe.shape_c(BASE.replace(T=0)))
     assert L.moe_permute_noalloc(z, None, None, None, None, None, None, None, None) == moe.MOE_OK
+
+
+def test_missing_library_fails_loudly():
+    """With the HIP library absent the binding raises: there is no other path to fall back to.
+    Run in a fresh process so this process's loaded library is untouched."""
+    import subprocess
+    import sys
+    code = ("from paper_2607_18631_amd import moe\n"
+            "moe.LIB_PATH = '/nonexistent/libmoe_mi355x.so'\n"
+            "try:\n"
+            "    moe.lib()\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n"
+            "    raise SystemExit(0)\n"
+            "raise SystemExit(3)\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
+    assert "is missing" in r.stdout
